@@ -1,0 +1,255 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused Tetra decode-GEMV on one MI355X.
+
+A step is one token-equivalent pass over the weight matrices of a
+Qwen3-shaped model at batch 1: every projection (q, k, v, o, gate, up, down)
+of every layer runs once through tetra_gemv on one stream (captured in a HIP
+graph so host launch cost is not timed).  The default workload is the
+Qwen3-14B shape set x 40 layers (280 matrices, 3.34 GB of codes), larger
+than the 256 MB last-level cache, so every step streams from HBM.
+
+Inputs are synthetic and seeded: uniformly random code bytes (every 48-bit
+word is legal), fp16 row scales U(0.5, 2) * 1e-2, fp16 tails N(0, 1) * sigma,
+fp16 activations N(0, 1).  All buffers are resident in HBM before timing.
+
+Prints one JSON line (rank 0, N = 1):
+  value    = algorithmic bytes per step / wall time per step (GB/s)
+  roofline = bytes / summed kernel time of the gemv launches (HIP events
+             on the launch stream), against the 8 TB/s HBM peak
+  cpu_baseline = the CPU oracle on a bounded sample of the same workload
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "Tetra GEMV achieved HBM GB/s (% of peak) and bits read/weight, batch 1"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--model", default="14B", choices=["4B", "8B", "14B"])
+    ap.add_argument("--layers", type=int, default=0, help="0 = all layers of the model")
+    ap.add_argument("--batch", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+class Matrix:
+    """One packed Tetra projection resident on the GPU."""
+
+    def __init__(self, torch, tt, name, M, K, gen, seed):
+        self.name, self.M, self.K = name, M, K
+        self.nblk, self.T = K // 24, K % 24
+        nbytes = tt.codes_bytes(M, K)
+        toff = tt.tail_offset(M, K)
+        self.blob = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        # any byte string is a legal code region (every 48-bit word is legal)
+        self.blob[:toff].random_(0, 256, generator=gen)
+        self.blob[toff:].zero_()
+        g = torch.Generator(device="cuda").manual_seed(seed)
+        self.sigma = (torch.rand(M, generator=g, device="cuda") * 1.5 + 0.5).mul_(1e-2).half()
+        if self.T:
+            tail = (torch.randn(M, self.T, generator=g, device="cuda") *
+                    self.sigma.float()[:, None]).half()
+            self.blob[toff:toff + 2 * M * self.T].copy_(tail.view(torch.uint8).reshape(-1))
+        # bytes the kernel must read: code chunks, tail, row scales
+        self.code_bytes = toff
+        self.read_bytes = (M // 64) * self.nblk * 384 + (M % 64 > 0) * self.nblk * 384 \
+            + 2 * M * self.T + 2 * M
+        self.weights = M * K
+
+
+def build_workload(torch, tt, model, layers, batch):
+    from paper_2609_35465_amd import workloads
+    shapes = workloads.layer_shapes(model)
+    L = layers or workloads.QWEN3[model]["layers"]
+    gen = torch.Generator(device="cuda").manual_seed(workloads.SEED_BASE + 3)
+    mats, xs, ys = [], {}, []
+    for layer in range(L):
+        for i, (name, M, K) in enumerate(shapes):
+            mats.append(Matrix(torch, tt, name, M, K, gen, workloads.seed_for(3, 16 * layer + i)))
+            if (layer, K) not in xs:
+                xs[(layer, K)] = torch.randn(batch, K, generator=gen, device="cuda").half()
+            ys.append(torch.empty(batch, M, dtype=torch.float32, device="cuda"))
+    plan = [(m, xs[(li // len(shapes), m.K)], ys[li]) for li, m in enumerate(mats)]
+    return plan, L
+
+
+def run_step(tt, plan, batch, stream):
+    for m, x, y in plan:
+        tt.gemv(m.blob, m.sigma, x, y, m.M, m.K, batch, stream)
+
+
+def parity_spot_check(torch, tt, plan, batch):
+    """Sampled rows of the first matrices of each shape against the oracle."""
+    from oracle import gemv as ogemv
+    worst = 0.0
+    seen = set()
+    for m, x, y in plan:
+        if m.name in seen:
+            continue
+        seen.add(m.name)
+        rows = np.unique(np.r_[0:8, m.M - 8:m.M, np.linspace(0, m.M - 1, 24).astype(int)])
+        blob = m.blob.cpu().numpy()
+        words, tail = tt.unpack_rows(blob, m.M, m.K)
+        sig = m.sigma.cpu().numpy()
+        xh = x.cpu().numpy()
+        ref, norm = ogemv.gemv_f64(words, sig, tail, xh, rows=rows)
+        got = y.cpu().numpy()[:, rows].astype(np.float64)
+        worst = max(worst, float((np.abs(got - ref) / norm).max()))
+    return worst
+
+
+def cpu_baseline(torch, tt, plan, seconds):
+    """The CPU oracle (numpy, one thread) on rows of the largest matrix,
+    grown until it has run for `seconds`; rate in GB/s of Tetra bytes."""
+    from oracle import gemv as ogemv
+    m, x, _ = max(plan, key=lambda p: p[0].M * p[0].K)
+    blob = m.blob.cpu().numpy()
+    words, tail = tt.unpack_rows(blob, m.M, m.K)
+    sig = m.sigma.cpu().numpy()
+    xh = x.cpu().numpy()
+    rows_done, t_used, n = 0, 0.0, 16
+    while t_used < seconds and rows_done < m.M:
+        rows = np.arange(rows_done, min(rows_done + n, m.M))
+        t0 = time.perf_counter()
+        ogemv.gemv_f64(words, sig, tail, xh, rows=rows)
+        t_used += time.perf_counter() - t0
+        rows_done += len(rows)
+        n *= 2
+    bytes_done = rows_done * (m.nblk * 6 + 2 * m.T + 2)
+    return {
+        "value": round(bytes_done / t_used / 1e9, 6), "unit": "GB/s", "cores": 1,
+        "kind": "oracle",
+        "sample": f"{rows_done} rows of the {m.M}x{m.K} {m.name} matrix "
+                  f"({rows_done * m.nblk} blocks) in {t_used:.1f} s, float64 numpy",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the fused GEMV has no multi-GPU path in "
+              "this build (rows shard without communication; see the design notes). "
+              "Run with --gpus 1.", file=sys.stderr)
+        return 2
+    import torch
+    import paper_2609_35465_amd as tt
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    plan, L = build_workload(torch, tt, args.model, args.layers, args.batch)
+    torch.cuda.synchronize()
+
+    bytes_read = sum(m.read_bytes for m, _, _ in plan)
+    bytes_xy = sum(2 * m.K * args.batch + 4 * m.M * args.batch for m, _, _ in plan)
+    weights = sum(m.weights for m, _, _ in plan)
+    algo_bytes = bytes_read + bytes_xy
+
+    # warm-up (also uploads the decoder tables)
+    for _ in range(max(1, args.warmup)):
+        run_step(tt, plan, args.batch, stream.cuda_stream)
+    torch.cuda.synchronize()
+    parity = parity_spot_check(torch, tt, plan, args.batch)
+
+    graph = None
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            run_step(tt, plan, args.batch, torch.cuda.current_stream().cuda_stream)
+        # replays must reproduce the eager result
+        ref = [y.clone() for _, _, y in plan[:7]]
+        for _ in range(3):
+            for _, _, y in plan[:7]:
+                y.zero_()
+            graph.replay()
+            torch.cuda.synchronize()
+            for r, (_, _, y) in zip(ref, plan[:7]):
+                assert torch.equal(r, y), "graph replay differs from the eager run"
+
+    def step():
+        if graph is not None:
+            graph.replay()
+        else:
+            run_step(tt, plan, args.batch, stream.cuda_stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+
+    # per-launch kernel time: events around every launch on the launch stream
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in plan]
+    for (a, b), (m, x, y) in zip(evs, plan):
+        a.record(stream)
+        tt.gemv(m.blob, m.sigma, x, y, m.M, m.K, args.batch, stream.cuda_stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    kern_ms = sum(a.elapsed_time(b) for a, b in evs)
+    avg_launch_ms = kern_ms / len(plan)
+    achieved = (algo_bytes / len(plan)) / (avg_launch_ms * 1e-3) / 1e9
+
+    value = algo_bytes / (ms_step * 1e-3) / 1e9
+    bits_w = bytes_read * 8 / weights
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16-in/f32-acc",
+        "data": "synthetic",
+        "config": {
+            "workload": f"Qwen3-{args.model}-shaped linear set x {L} layers "
+                        f"({len(plan)} Tetra matrices), batch {args.batch}, one token-equivalent pass",
+            "batch": args.batch, "layers": L, "matrices": len(plan),
+            "hip_graph": graph is not None,
+        },
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "bits_read_per_weight": round(bits_w, 4),
+        "weights_per_s": round(weights / (ms_step * 1e-3), 1),
+        "token_equiv_latency_ms": round(ms_step, 4),
+        "parity_worst_rel_err": parity,
+        "roofline": {
+            "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "kernel": "gemv_kernel", "avg_launch_us": round(avg_launch_ms * 1e3, 3),
+            "bytes_per_launch": round(algo_bytes / len(plan)),
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(torch, tt, plan, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,153 @@
+/*
+ * tetra.h - C ABI of the MI355X (gfx950) Tetra decode and fused decode-GEMV.
+ *
+ * The method: each block of 24 weights is one 48-bit code (Sec. 3.3-3.4 and
+ * Fig. 3-4 of "Tetra: Serving Leech-Lattice Quantized LLMs at 2.7 Bits per
+ * Parameter").  A code names a path through the 64-state trellis of the
+ * Golay code in octad order (Sec. 3.2), a shared parity p, the k-parity r of
+ * section 1, a gain bit g and three 11-bit indices into one table of 4,096
+ * rank vectors; the decoded block is a point y of the Leech lattice (Eq. 1)
+ * and the weights are w_j = y_j / sqrt(16 m) * gain[g] * sigma_row (Eq. 2).
+ * The fused product y = W x never writes W (Sec. 5.1).
+ *
+ * Conventions fixed by this library where the paper is silent (the word bit
+ * layout, the trellis numbering, the rank-table tie-break, the value order
+ * for o = 2 and the gain values) are the canonical ones returned by
+ * tetra_get_tables() and documented with the design notes.
+ *
+ * Canonical 48-bit word, stored as 6 little-endian bytes:
+ *     bits 0-5 s8 | 6 p | 7 r | 8 b1 | 9-12 b2 | 13 b3 | 14 g |
+ *     15-25 i1 | 26-36 i2 | 37-47 i3
+ * Every 48-bit value is a legal word.
+ *
+ * Memory: all buffers are owned by the caller.  "host" arguments are plain
+ * host pointers; "device" arguments are device pointers on the current HIP
+ * device (for example from hipMalloc or torch.empty(..., device="cuda")).
+ * The library owns only its constant decoder tables, uploaded once per
+ * device on first use (thread-safe).  Launching calls are asynchronous on
+ * the given stream, never synchronise and never allocate.
+ *
+ * Errors: every call validates its arguments before any launch and returns
+ * a tetra_status.  TETRA_EDEVICE reports a HIP error seen at launch time;
+ * faults inside a kernel surface at the caller's next synchronisation.
+ */
+#ifndef TETRA_H
+#define TETRA_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TETRA_OK = 0,
+    TETRA_EINVAL = -1,       /* null pointer, size out of range, bad batch  */
+    TETRA_EALIGN = -2,       /* a device pointer is not aligned as required */
+    TETRA_EDEVICE = -3,      /* HIP runtime error (table upload or launch)  */
+    TETRA_EUNSUPPORTED = -4  /* valid request this build does not serve     */
+} tetra_status;
+
+/* Rows of one code tile of the device layout (see tetra_pack_rows). */
+#define TETRA_ROW_TILE 64
+/* Bytes of the canonical table blob returned by tetra_get_tables. */
+#define TETRA_TABLE_BLOB_BYTES 18824
+/* Largest batch (number of activation vectors) served by tetra_gemv. */
+#define TETRA_MAX_BATCH 8
+
+/* Message for a status code (static string, never NULL). */
+const char* tetra_status_string(int status);
+
+/*
+ * Canonical decoder tables (Fig. 4; Sec. 3.3-3.4), little-endian:
+ *   rows u32[4096] | branches u16[1024] | prefixes u8[128] |
+ *   suffixes u8[128] | invnorm f32[32] | gain f32[2]
+ * 16,384 + 2,048 + 128 + 128 + 128 + 8 = 18,824 bytes: the paper's
+ * 18,816 B of rank rows, trellis tables and 1/sqrt(16m), plus the two gains.
+ * rows: the 2,048 cheapest rank vectors of class 0 then of class 1
+ * (nibble j = rank of section coordinate j).  branches[16*s8+b2] =
+ * P2 | s16 << 8.  Host only; out: host buffer of at least
+ * TETRA_TABLE_BLOB_BYTES.  Returns TETRA_EINVAL if out is NULL or bytes is
+ * too small.
+ */
+int tetra_get_tables(void* out, size_t bytes);
+
+/*
+ * Size in bytes of the device code blob of an M x K Tetra matrix.
+ * K splits into nblk = K / 24 code blocks and an unquantised tail of
+ * T = K % 24 weights per row (Sec. 4.1).  Returns 0 if M < 1, K < 24 or K
+ * is odd.
+ */
+size_t tetra_codes_bytes(int M, int K);
+
+/* Byte offset of the fp16 tail inside the code blob (0 if the shape is
+ * invalid): the code chunks rounded up to 16 bytes. */
+size_t tetra_tail_offset(int M, int K);
+
+/*
+ * Host packer (the loader step of Sec. 5.1: it reorders code words, it
+ * expands nothing).  words: host uint64[M][nblk], canonical words in the low
+ * 48 bits (upper bits must be 0).  tail: host fp16 bits [M][T], may be NULL
+ * iff T == 0.  out: host buffer of tetra_codes_bytes(M, K) bytes.
+ *
+ * Device layout (ours): rows are grouped in tiles of TETRA_ROW_TILE rows
+ * (the last tile padded with zero words, which decode to the origin).  For
+ * tile t and block column b, a 384-byte chunk at offset (t*nblk + b)*384
+ * holds the low 32 bits of the 64 words (row-in-tile order), then their
+ * high 16 bits.  The fp16 tail follows, row-major [M][T], starting at a
+ * 16-byte aligned offset.  Bits read per weight: 48 per block plus 16 per
+ * tail weight (plus the fp16 row scale passed separately).
+ * Returns TETRA_EINVAL on a NULL pointer, a bad shape, a word with bits
+ * above 47 set, or out_bytes < tetra_codes_bytes(M, K).
+ */
+int tetra_pack_rows(const uint64_t* words, const uint16_t* tail, int M, int K,
+                    void* out, size_t out_bytes);
+
+/* Inverse of tetra_pack_rows (host only, for checks). */
+int tetra_unpack_rows(const void* codes, size_t codes_bytes, int M, int K,
+                      uint64_t* words, uint16_t* tail);
+
+/*
+ * Fused decode and matrix-vector product (Sec. 5.1, Eq. 2):
+ *   y[b][row] = sigma_row * sum_blk s_blk * sum_j y_j x[b][24*blk + j]
+ *               + sum_t tail[row][t] * x[b][24*nblk + t]
+ * with s_blk = gain[g] * (1/sqrt(16 m)) in f32 and f32 accumulation.
+ *   codes:      device, tetra_pack_rows layout, 16-byte aligned
+ *   row_scales: device fp16[M] (sigma_row)
+ *   x:          device fp16[batch][K], 4-byte aligned
+ *   y:          device fp32[batch][M], fully overwritten
+ *   batch:      1..TETRA_MAX_BATCH
+ * Asynchronous on stream.  TETRA_EINVAL for NULL pointers, bad M/K, batch
+ * out of range; TETRA_EALIGN for misaligned codes or x; TETRA_EDEVICE when
+ * the table upload or the launch fails.
+ */
+int tetra_gemv(const void* codes, const uint16_t* row_scales, const uint16_t* x,
+               float* y, int M, int K, int batch, hipStream_t stream);
+
+/*
+ * Bulk decode of n canonical words (Sec. 3.4, Fig. 4), for testing.
+ *   words:         device, n*6 bytes, canonical little-endian words
+ *   y_out:         device int8[n][24], the lattice point in block order
+ *   blk_scale_out: device fp32[n], s_blk = fl32(gain[g] * invnorm[m]);
+ *                  may be NULL
+ * Asynchronous.  TETRA_EINVAL for NULL words/y_out or n == 0.
+ */
+int tetra_decode(const void* words, size_t n, int8_t* y_out, float* blk_scale_out,
+                 hipStream_t stream);
+
+/*
+ * Dense reconstruction of a packed matrix (Eq. 2), for testing:
+ *   w_out[row][24*blk+j] = fl32(fl32(y_j * s_blk) * sigma_row),
+ *   w_out[row][24*nblk+t] = tail[row][t].
+ *   codes / row_scales as in tetra_gemv; w_out: device fp32[M][K].
+ */
+int tetra_dequant(const void* codes, const uint16_t* row_scales, int M, int K,
+                  float* w_out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TETRA_H */

@@ -1,0 +1,145 @@
+"""Python binding of libtetra.so (the MI355X Tetra decode-GEMV library).
+
+Argument marshalling only: every step of the decode and the product runs in
+the library's HIP kernels.  Device buffers are torch tensors on a ROCm
+device (torch is used for memory and streams only); host-side helpers take
+numpy arrays.  The first call loads libtetra.so, built in-tree by
+``paper_2609_35465_amd.build``; a missing library raises ImportError.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtetra.so")
+
+OK, EINVAL, EALIGN, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4
+ROW_TILE = 64
+TABLE_BLOB_BYTES = 18824
+MAX_BATCH = 8
+
+_vp, _sz, _int = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+
+# name: (restype, argtypes)
+_SIGNATURES = {
+    "tetra_status_string": (ctypes.c_char_p, [_int]),
+    "tetra_get_tables": (_int, [_vp, _sz]),
+    "tetra_codes_bytes": (_sz, [_int, _int]),
+    "tetra_tail_offset": (_sz, [_int, _int]),
+    "tetra_pack_rows": (_int, [_vp, _vp, _int, _int, _vp, _sz]),
+    "tetra_unpack_rows": (_int, [_vp, _sz, _int, _int, _vp, _vp]),
+    "tetra_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
+    "tetra_decode": (_int, [_vp, _sz, _vp, _vp, _vp]),
+    "tetra_dequant": (_int, [_vp, _vp, _int, _int, _vp, _vp]),
+}
+EXPORTED = tuple(_SIGNATURES)
+
+_lib = None
+
+
+def library():
+    """The loaded ctypes library (loaded on first use; raises if it is
+    missing, so no call can silently fall back to another implementation)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2609_35465_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            f = getattr(lib, name)
+            f.restype, f.argtypes = res, args
+        _lib = lib
+    return _lib
+
+
+def _call(name, *args):
+    return getattr(library(), name)(*args)
+
+
+class TetraError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+
+
+def status_string(status: int) -> str:
+    return _call("tetra_status_string", status).decode()
+
+
+def _check(status, what):
+    if status != OK:
+        raise TetraError(status, what)
+
+
+# ------------------------------------------------------------------ host side
+
+def get_tables() -> bytes:
+    buf = ctypes.create_string_buffer(TABLE_BLOB_BYTES)
+    _check(_call("tetra_get_tables", buf, TABLE_BLOB_BYTES), "tetra_get_tables")
+    return buf.raw
+
+
+def codes_bytes(M: int, K: int) -> int:
+    return int(_call("tetra_codes_bytes", M, K))
+
+
+def tail_offset(M: int, K: int) -> int:
+    return int(_call("tetra_tail_offset", M, K))
+
+
+def pack_rows(words: np.ndarray, tail: np.ndarray, M: int, K: int) -> np.ndarray:
+    """Device code blob (as a host uint8 array) of canonical words
+    uint64 [M, K//24] and fp16 tail [M, K%24]."""
+    words = np.ascontiguousarray(words, dtype=np.uint64)
+    n = codes_bytes(M, K)
+    if n == 0:
+        raise TetraError(EINVAL, "tetra_codes_bytes")
+    out = np.zeros(n, dtype=np.uint8)
+    tptr = None
+    if K % 24:
+        tail = np.ascontiguousarray(tail, dtype=np.float16)
+        tptr = tail.ctypes.data
+    _check(_call("tetra_pack_rows", words.ctypes.data, tptr, M, K, out.ctypes.data, n), "tetra_pack_rows")
+    return out
+
+
+def unpack_rows(codes: np.ndarray, M: int, K: int):
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    words = np.zeros((M, K // 24), dtype=np.uint64)
+    tail = np.zeros((M, K % 24), dtype=np.float16)
+    _check(_call("tetra_unpack_rows", codes.ctypes.data, codes.nbytes, M, K, words.ctypes.data,
+                       tail.ctypes.data if K % 24 else None), "tetra_unpack_rows")
+    return words, tail
+
+
+# ---------------------------------------------------------------- device side
+
+def _stream(stream):
+    if stream is not None:
+        return stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def gemv(codes, row_scales, x, y, M: int, K: int, batch: int = 1, stream=None):
+    """y[batch, M] = W x for a packed Tetra matrix (all device tensors)."""
+    _check(_call("tetra_gemv", _ptr(codes), _ptr(row_scales), _ptr(x), _ptr(y), M, K, batch,
+                     _stream(stream)), "tetra_gemv")
+
+
+def decode(words_bytes, n: int, y_out, scale_out=None, stream=None):
+    """words_bytes: device uint8 [n*6]; y_out int8 [n, 24]; scale_out f32 [n]."""
+    _check(_call("tetra_decode", _ptr(words_bytes), n, _ptr(y_out), _ptr(scale_out),
+                       _stream(stream)), "tetra_decode")
+
+
+def dequant(codes, row_scales, M: int, K: int, w_out, stream=None):
+    _check(_call("tetra_dequant", _ptr(codes), _ptr(row_scales), M, K, _ptr(w_out),
+                        _stream(stream)), "tetra_dequant")

@@ -1,0 +1,203 @@
+"""GPU parity of the HIP path against the CPU oracle (run on an MI355X).
+
+Bars:
+* decode and dequant: bit-exact (int8 coordinates, f32 block scales and
+  weights);
+* GEMV: max over rows of |y_gpu - y_ref| / sum_k |w_k x_k| <= 1e-3, with
+  y_ref the oracle's float64 product; a stricter 1e-5 (the paper's own
+  per-row bound) is asserted too, since the kernel accumulates in f32.
+
+Every call goes through the C ABI via the ctypes binding.
+"""
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+import paper_2609_35465_amd as tt  # noqa: E402
+from paper_2609_35465_amd import workloads  # noqa: E402
+from oracle import codec, gemv as ogemv  # noqa: E402
+
+TOL = 1e-3
+TOL_PAPER = 1e-5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    torch.cuda.init()
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _f16_dev(a):
+    return _dev(np.ascontiguousarray(a, dtype=np.float16))
+
+
+class Packed:
+    def __init__(self, words, sigma, tail, K):
+        self.M, self.K = words.shape[0], K
+        self.blob = _dev(tt.pack_rows(words, tail, self.M, K))
+        self.sigma = _f16_dev(sigma)
+        self.words, self.sigma_h, self.tail = words, sigma, tail
+
+    def gemv(self, x):
+        batch = x.shape[0]
+        xd = _f16_dev(x)
+        y = torch.empty((batch, self.M), dtype=torch.float32, device="cuda")
+        tt.gemv(self.blob, self.sigma, xd, y, self.M, self.K, batch)
+        torch.cuda.synchronize()
+        return y.cpu().numpy()
+
+
+def _check_gemv(pk, x, rows=None, label=""):
+    yg = pk.gemv(x)
+    yr, norm = ogemv.gemv_f64(pk.words, pk.sigma_h, pk.tail, x, rows=rows)
+    if rows is not None:
+        yg = yg[:, rows]
+    err = np.abs(yg.astype(np.float64) - yr) / np.maximum(norm, 1e-300)
+    worst = float(err.max())
+    print(f"[gemv {label}] M={pk.M} K={pk.K} batch={x.shape[0]} worst={worst:.3e}", flush=True)
+    assert worst <= TOL
+    assert worst <= TOL_PAPER
+    return yg
+
+
+# ------------------------------------------------------------------ decode
+
+def _special_words():
+    f = codec.FIELDS
+    out = [0, (1 << 48) - 1]
+    for name, (lsb, n) in f.items():
+        out.append(((1 << n) - 1) << lsb)                 # field at its maximum
+        out.append(((1 << 48) - 1) ^ (((1 << n) - 1) << lsb))
+    # the i2 boundary between the class-0 and class-1 parts of the middle list
+    for i2 in (1239, 1240, 2047):
+        out.append(i2 << 26)
+    return np.array(out, dtype=np.uint64)
+
+
+@pytest.mark.parametrize("n", [1, 7, 1 << 20])
+def test_decode_bit_exact(n):
+    rng = np.random.default_rng(n)
+    words = rng.integers(0, 1 << 48, size=n, dtype=np.uint64)
+    if n > 100:
+        sp = _special_words()
+        words[:len(sp)] = sp
+    wb = codec.words_to_bytes(words).reshape(-1)
+    y = torch.empty((n, 24), dtype=torch.int8, device="cuda")
+    s = torch.empty(n, dtype=torch.float32, device="cuda")
+    print(f"[decode] n={n}", flush=True)
+    tt.decode(_dev(wb), n, y, s)
+    torch.cuda.synchronize()
+    yo, _, so = codec.decode(words)
+    assert np.array_equal(y.cpu().numpy(), yo)
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), so.view(np.uint32))
+
+
+def test_decode_without_scale_output():
+    words = np.arange(1000, dtype=np.uint64) * 0x10000000001
+    wb = codec.words_to_bytes(words).reshape(-1)
+    y = torch.empty((1000, 24), dtype=torch.int8, device="cuda")
+    tt.decode(_dev(wb), 1000, y, None)
+    torch.cuda.synchronize()
+    assert np.array_equal(y.cpu().numpy(), codec.decode(words)[0])
+
+
+# ----------------------------------------------------------------- dequant
+
+@pytest.mark.parametrize("M,K", [(1536, 1536), (100, 24 * 5 + 8), (1, 24), (65, 24 * 3 + 16)])
+def test_dequant_bit_exact(M, K):
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(0, M % 7), M, K)
+    pk = Packed(words, sigma, tail, K)
+    w = torch.empty((M, K), dtype=torch.float32, device="cuda")
+    print(f"[dequant] M={M} K={K}", flush=True)
+    tt.dequant(pk.blob, pk.sigma, M, K, w)
+    torch.cuda.synchronize()
+    ref = ogemv.dequant(words, sigma, tail)
+    assert np.array_equal(w.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
+# -------------------------------------------------------------------- GEMV
+
+SMALL_SHAPES = [
+    (1, 24), (64, 48), (63, 24 * 3 + 8), (65, 24 * 9 + 16), (127, 24 * 5),
+    (200, 24 * 64), (256, 2560), (130, 24 * 11 + 8), (1536, 1536),
+]
+
+
+@pytest.mark.parametrize("M,K", SMALL_SHAPES)
+def test_gemv_small_shapes(M, K):
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(0, 3) + M + K, M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(M + K, 1, K)
+    _check_gemv(pk, x, label="small")
+
+
+@pytest.mark.parametrize("batch", list(range(1, 9)))
+def test_gemv_batches(batch):
+    M, K = 192, 24 * 40 + 16
+    words, sigma, tail = workloads.tetra_matrix(123, M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(500 + batch, batch, K)
+    yb = _check_gemv(pk, x, label="batch")
+    # each batch row equals the batch-1 result for the same vector
+    for b in range(batch):
+        y1 = pk.gemv(x[b:b + 1])
+        assert np.array_equal(y1[0], yb[b])
+
+
+def test_gemv_degenerate_inputs():
+    M, K = 70, 24 * 4 + 8
+    words, sigma, tail = workloads.tetra_matrix(9, M, K)
+    # origin words: only the tail remains
+    pk = Packed(np.zeros_like(words), sigma, tail, K)
+    x = workloads.activations(9, 2, K)
+    yg = pk.gemv(x)
+    want = x[:, 96:].astype(np.float64) @ tail.astype(np.float64).T
+    assert np.allclose(yg, want, rtol=1e-5, atol=1e-6)
+    # zero activations give exact zeros
+    pk = Packed(words, sigma, tail, K)
+    assert not pk.gemv(np.zeros((1, K), np.float16)).any()
+    # a single nonzero activation picks one weight column
+    W = ogemv.dequant(words, sigma, tail)
+    for k in (0, 23, 24, 95, 96, 103):
+        e = np.zeros((1, K), np.float16)
+        e[0, k] = 1.0
+        assert np.allclose(pk.gemv(e)[0], W[:, k], rtol=1e-6, atol=0)
+
+
+def test_gemv_extreme_words():
+    """Rows of words at the corners of the code space (field maxima, the
+    middle-list boundary)."""
+    sp = _special_words()
+    M, K = 64, 24 * len(sp)
+    words = np.stack([np.roll(sp, r) for r in range(M)])
+    sigma = np.full(M, 0.0123, np.float16)
+    pk = Packed(words, sigma, np.zeros((M, 0), np.float16), K)
+    x = workloads.activations(77, 3, K)
+    _check_gemv(pk, x, label="extreme")
+
+
+# ----------------------------------------- full-size configurations (sampled)
+
+def _sample_rows(M, rng, n=192):
+    rows = set(range(min(M, 64))) | {M - 1, M - 2, M // 2}
+    rows |= set(rng.choice(M, size=min(n, M), replace=False).tolist())
+    return np.array(sorted(rows))
+
+
+@pytest.mark.parametrize("config,batch", [(0, 1), (1, 1), (2, 1), (3, 1), (3, 4)])
+def test_gemv_config_sampled_rows(config, batch):
+    rng = np.random.default_rng(config * 10 + batch)
+    for idx, (name, M, K) in enumerate(workloads.config_shapes(config)):
+        words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(config, idx), M, K)
+        pk = Packed(words, sigma, tail, K)
+        x = workloads.activations(workloads.seed_for(config, idx), batch, K)
+        _check_gemv(pk, x, rows=_sample_rows(M, rng), label=f"c{config}:{name}")
+        del pk

@@ -1,0 +1,126 @@
+"""Host-side checks of libtetra.so (no GPU needed).
+
+* the library loads and exports every function that include/tetra.h declares;
+* the library's own table builder (C++) gives byte for byte the oracle's
+  tables (the two are written independently from the same conventions);
+* pack/unpack round trips and the documented chunk layout;
+* argument validation returns the documented status codes before any launch.
+"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_35465_amd as tt
+from oracle import tables as otables
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "tetra.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tetra_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions()
+    assert len(names) >= 8
+    lib = tt.library()
+    for n in names:
+        assert hasattr(lib, n), n
+        assert isinstance(getattr(lib, n), ctypes._CFuncPtr)
+    assert set(names) == set(tt.EXPORTED)
+
+
+def test_tables_match_oracle_bytes():
+    blob = tt.get_tables()
+    assert len(blob) == tt.TABLE_BLOB_BYTES == otables.BLOB_BYTES
+    assert blob == otables.table_blob()
+
+
+def test_status_strings():
+    for s in (tt.OK, tt.EINVAL, tt.EALIGN, tt.EDEVICE, tt.EUNSUPPORTED):
+        assert tt.status_string(s)
+    assert tt.status_string(12345) == "unknown status"
+
+
+@pytest.mark.parametrize("M,K", [(1, 24), (64, 1536), (65, 24 * 7 + 8), (130, 2560), (17, 48)])
+def test_pack_unpack_round_trip(M, K):
+    rng = np.random.default_rng(M * 1000 + K)
+    words = rng.integers(0, 1 << 48, size=(M, K // 24), dtype=np.uint64)
+    tail = rng.standard_normal((M, K % 24)).astype(np.float16)
+    blob = tt.pack_rows(words, tail, M, K)
+    assert blob.nbytes == tt.codes_bytes(M, K)
+    w2, t2 = tt.unpack_rows(blob, M, K)
+    assert np.array_equal(w2, words)
+    assert np.array_equal(t2.view(np.uint16), tail.view(np.uint16))
+
+
+def test_pack_layout_is_the_documented_chunking():
+    M, K = 70, 24 * 3 + 16
+    nblk, T = 3, 16
+    rng = np.random.default_rng(3)
+    words = rng.integers(0, 1 << 48, size=(M, nblk), dtype=np.uint64)
+    tail = rng.standard_normal((M, T)).astype(np.float16)
+    blob = tt.pack_rows(words, tail, M, K)
+    tiles = 2
+    for row in (0, 5, 63, 64, 69):
+        tile, r = divmod(row, 64)
+        for b in range(nblk):
+            base = (tile * nblk + b) * 384
+            lo = int(blob[base + 4 * r: base + 4 * r + 4].view(np.uint32)[0])
+            hi = int(blob[base + 256 + 2 * r: base + 256 + 2 * r + 2].view(np.uint16)[0])
+            assert lo | (hi << 32) == int(words[row, b])
+    # padded rows of the last tile are zero words
+    base = (1 * nblk + 0) * 384
+    assert not blob[base + 4 * 6: base + 256].any()
+    tail_off = (tiles * nblk * 384 + 15) // 16 * 16
+    assert np.array_equal(blob[tail_off:].view(np.uint16).reshape(M, T), tail.view(np.uint16))
+
+
+def test_codes_bytes_and_bits_per_weight():
+    assert tt.codes_bytes(0, 24) == 0 and tt.codes_bytes(4, 23) == 0 and tt.codes_bytes(4, 25) == 0
+    # 48 bits per block + 16 per tail weight; + 16 per row for the fp16 scale
+    M, K = 5120, 17408
+    n = tt.codes_bytes(M, K)
+    assert n == (M // 64) * (K // 24) * 384 + M * (K % 24) * 2
+    bw = (n + 2 * M) * 8 / (M * K)
+    assert 2.0 < bw < 2.2
+
+
+def test_pack_rejects_bad_input():
+    words = np.zeros((2, 1), np.uint64)
+    words[1, 0] = 1 << 48
+    with pytest.raises(tt.TetraError) as e:
+        tt.pack_rows(words, None, 2, 24)
+    assert e.value.status == tt.EINVAL
+    lib = tt.library()
+    assert lib.tetra_pack_rows(None, None, 2, 24, None, 0) == tt.EINVAL
+    buf = np.zeros(10, np.uint8)
+    ok = np.zeros((2, 1), np.uint64)
+    assert lib.tetra_pack_rows(ok.ctypes.data, None, 2, 24, buf.ctypes.data, 10) == tt.EINVAL
+    # a tail is required when K % 24 != 0
+    big = np.zeros(tt.codes_bytes(2, 40), np.uint8)
+    w1 = np.zeros((2, 1), np.uint64)
+    assert lib.tetra_pack_rows(w1.ctypes.data, None, 2, 40, big.ctypes.data, big.nbytes) == tt.EINVAL
+
+
+def test_launch_entry_points_validate_before_touching_the_device():
+    lib = tt.library()
+    fake = 0x1000                   # never dereferenced: validation fails first
+    assert lib.tetra_gemv(None, fake, fake, fake, 64, 48, 1, None) == tt.EINVAL
+    assert lib.tetra_gemv(fake, fake, fake, fake, 0, 48, 1, None) == tt.EINVAL
+    assert lib.tetra_gemv(fake, fake, fake, fake, 64, 23, 1, None) == tt.EINVAL
+    assert lib.tetra_gemv(fake, fake, fake, fake, 64, 48, 0, None) == tt.EINVAL
+    assert lib.tetra_gemv(fake, fake, fake, fake, 64, 48, 9, None) == tt.EINVAL
+    assert lib.tetra_gemv(fake + 4, fake, fake, fake, 64, 48, 1, None) == tt.EALIGN
+    assert lib.tetra_gemv(fake, fake, fake + 2, fake, 64, 48, 1, None) == tt.EALIGN
+    assert lib.tetra_decode(None, 10, fake, None, None) == tt.EINVAL
+    assert lib.tetra_decode(fake, 0, fake, None, None) == tt.EINVAL
+    assert lib.tetra_decode(fake + 1, 4, fake, None, None) == tt.EALIGN
+    assert lib.tetra_dequant(fake, None, 64, 48, fake, None) == tt.EINVAL
+    assert lib.tetra_dequant(fake + 8, fake, 64, 48, fake, None) == tt.EALIGN
