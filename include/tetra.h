@@ -93,12 +93,19 @@ size_t tetra_tail_offset(int M, int K);
  * iff T == 0.  out: host buffer of tetra_codes_bytes(M, K) bytes.
  *
  * Device layout (ours): rows are grouped in tiles of TETRA_ROW_TILE rows
- * (the last tile padded with zero words, which decode to the origin).  For
- * tile t and block column b, a 384-byte chunk at offset (t*nblk + b)*384
- * holds the low 32 bits of the 64 words (row-in-tile order), then their
- * high 16 bits.  The fp16 tail follows, row-major [M][T], starting at a
- * 16-byte aligned offset.  Bits read per weight: 48 per block plus 16 per
- * tail weight (plus the fp16 row scale passed separately).
+ * (the last tile padded with the zero word, which decodes to the origin).
+ * For tile t and block column b, a 384-byte chunk at offset (t*nblk + b)*384
+ * holds 32 bits of each of the 64 words (row-in-tile order), then their
+ * other 16 bits.  Each word is stored recoded, still 48 bits and one-to-one
+ * with the canonical word: path = s8 | b1<<6 | b2<<7 | b3<<11, g, the
+ * physical rank-table row of section 1, i2, and section 3's physical row
+ * without delta, (p^r)<<11 | i3' (rank rows of class 0 sit at
+ * (i+808) mod 2048, of class 1 at 2048+i, so the middle list is 808+i2):
+ *   lo32 = path | g<<12 | phys1<<13 | (i2 & 0x7F)<<25,
+ *   hi16 = (i2 >> 7) | u3<<4.
+ * The fp16 tail follows, row-major [M][T], at a 16-byte aligned offset.
+ * Bits read per weight: 48 per block plus 16 per tail weight (plus the
+ * fp16 row scale passed separately).
  * Returns TETRA_EINVAL on a NULL pointer, a bad shape, a word with bits
  * above 47 set, or out_bytes < tetra_codes_bytes(M, K).
  */
@@ -125,6 +132,29 @@ int tetra_unpack_rows(const void* codes, size_t codes_bytes, int M, int K,
  */
 int tetra_gemv(const void* codes, const uint16_t* row_scales, const uint16_t* x,
                float* y, int M, int K, int batch, hipStream_t stream);
+
+/* Largest number of matrices in one tetra_gemv_grouped call. */
+#define TETRA_MAX_GROUP 16
+
+/* One matrix of a grouped product: arguments as in tetra_gemv. */
+typedef struct {
+    const void* codes;
+    const uint16_t* row_scales;
+    const uint16_t* x;
+    float* y;
+    int M, K;
+} tetra_gemv_problem;
+
+/*
+ * Several independent Tetra products in one launch (for instance the q, k
+ * and v projections that share an input, or all projections of a layer):
+ * problems[i].y = W_i problems[i].x for i < n, each exactly as tetra_gemv
+ * computes it.  problems: host array of n (1..TETRA_MAX_GROUP) entries,
+ * read during the call only.  Same status codes as tetra_gemv; a bad entry
+ * fails the whole call before any launch.
+ */
+int tetra_gemv_grouped(const tetra_gemv_problem* problems, int n, int batch,
+                       hipStream_t stream);
 
 /*
  * Bulk decode of n canonical words (Sec. 3.4, Fig. 4), for testing.

@@ -19,6 +19,7 @@ OK, EINVAL, EALIGN, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4
 ROW_TILE = 64
 TABLE_BLOB_BYTES = 18824
 MAX_BATCH = 8
+MAX_GROUP = 16
 
 _vp, _sz, _int = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
 
@@ -31,6 +32,7 @@ _SIGNATURES = {
     "tetra_pack_rows": (_int, [_vp, _vp, _int, _int, _vp, _sz]),
     "tetra_unpack_rows": (_int, [_vp, _sz, _int, _int, _vp, _vp]),
     "tetra_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
+    "tetra_gemv_grouped": (_int, [_vp, _int, _int, _vp]),
     "tetra_decode": (_int, [_vp, _sz, _vp, _vp, _vp]),
     "tetra_dequant": (_int, [_vp, _vp, _int, _int, _vp, _vp]),
 }
@@ -132,6 +134,27 @@ def gemv(codes, row_scales, x, y, M: int, K: int, batch: int = 1, stream=None):
     """y[batch, M] = W x for a packed Tetra matrix (all device tensors)."""
     _check(_call("tetra_gemv", _ptr(codes), _ptr(row_scales), _ptr(x), _ptr(y), M, K, batch,
                      _stream(stream)), "tetra_gemv")
+
+
+class Problem(ctypes.Structure):
+    """tetra_gemv_problem"""
+    _fields_ = [("codes", ctypes.c_void_p), ("row_scales", ctypes.c_void_p),
+                ("x", ctypes.c_void_p), ("y", ctypes.c_void_p),
+                ("M", ctypes.c_int), ("K", ctypes.c_int)]
+
+
+def make_problems(items):
+    """items: [(codes, row_scales, x, y, M, K)] of device tensors -> C array."""
+    arr = (Problem * len(items))()
+    for i, (c, s, x, y, M, K) in enumerate(items):
+        arr[i] = Problem(_ptr(c), _ptr(s), _ptr(x), _ptr(y), M, K)
+    return arr
+
+
+def gemv_grouped(problems, batch: int = 1, stream=None):
+    """Several products in one launch; problems from make_problems()."""
+    _check(_call("tetra_gemv_grouped", ctypes.cast(problems, ctypes.c_void_p), len(problems),
+                 batch, _stream(stream)), "tetra_gemv_grouped")
 
 
 def decode(words_bytes, n: int, y_out, scale_out=None, stream=None):

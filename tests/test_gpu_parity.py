@@ -184,6 +184,48 @@ def test_gemv_extreme_words():
     _check_gemv(pk, x, label="extreme")
 
 
+def test_gemv_grouped_matches_oracle():
+    """One launch over matrices of different shapes (ragged M, tails 0/8/16,
+    a single-block K) and different activations."""
+    shapes = [(100, 24 * 7 + 8), (64, 24), (257, 24 * 33 + 16), (1, 48), (640, 2560)]
+    for batch in (1, 3):
+        items, pks, xs = [], [], []
+        for i, (M, K) in enumerate(shapes):
+            words, sigma, tail = workloads.tetra_matrix(4000 + i, M, K)
+            pk = Packed(words, sigma, tail, K)
+            x = workloads.activations(4100 + i, batch, K)
+            xd = _f16_dev(x)
+            y = torch.full((batch, M), float("nan"), dtype=torch.float32, device="cuda")
+            items.append((pk.blob, pk.sigma, xd, y, M, K))
+            pks.append(pk)
+            xs.append(x)
+        probs = tt.make_problems(items)
+        print(f"[grouped] n={len(shapes)} batch={batch}", flush=True)
+        tt.gemv_grouped(probs, batch)
+        torch.cuda.synchronize()
+        for (blob, sg, xd, y, M, K), pk, x in zip(items, pks, xs):
+            yr, norm = ogemv.gemv_f64(pk.words, pk.sigma_h, pk.tail, x)
+            err = np.abs(y.cpu().numpy().astype(np.float64) - yr) / norm
+            assert float(err.max()) <= TOL_PAPER, (M, K, float(err.max()))
+
+
+def test_gemv_grouped_sixteen_problems():
+    items, refs = [], []
+    for i in range(16):
+        M, K = 64 + 37 * i, 24 * (3 + i) + (8 if i % 2 else 0)
+        words, sigma, tail = workloads.tetra_matrix(5000 + i, M, K)
+        pk = Packed(words, sigma, tail, K)
+        x = workloads.activations(5100 + i, 1, K)
+        y = torch.empty((1, M), dtype=torch.float32, device="cuda")
+        items.append((pk.blob, pk.sigma, _f16_dev(x), y, M, K))
+        refs.append((pk, x))
+    tt.gemv_grouped(tt.make_problems(items), 1)
+    torch.cuda.synchronize()
+    for (_, _, _, y, M, K), (pk, x) in zip(items, refs):
+        yr, norm = ogemv.gemv_f64(pk.words, pk.sigma_h, pk.tail, x)
+        assert float((np.abs(y.cpu().numpy() - yr) / norm).max()) <= TOL_PAPER
+
+
 # ----------------------------------------- full-size configurations (sampled)
 
 def _sample_rows(M, rng, n=192):

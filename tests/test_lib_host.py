@@ -60,26 +60,62 @@ def test_pack_unpack_round_trip(M, K):
     assert np.array_equal(t2.view(np.uint16), tail.view(np.uint16))
 
 
+def _device_word(w: int):
+    """The recoding documented in include/tetra.h, written out again here."""
+    f = {k: (w >> lsb) & ((1 << n) - 1) for k, (lsb, n) in {
+        "s8": (0, 6), "p": (6, 1), "r": (7, 1), "b1": (8, 1), "b2": (9, 4), "b3": (13, 1),
+        "g": (14, 1), "i1": (15, 11), "i2": (26, 11), "i3": (37, 11)}.items()}
+
+    def phys(cls, i):
+        return 2048 + i if cls else (i + 808) % 2048
+
+    delta = int(f["i2"] >= 1240)
+    r3 = f["p"] ^ f["r"] ^ delta
+    path = f["s8"] | f["b1"] << 6 | f["b2"] << 7 | f["b3"] << 11
+    phys1 = phys(f["r"], f["i1"])
+    u3 = phys(r3, f["i3"]) ^ (delta << 11)
+    lo = path | f["g"] << 12 | phys1 << 13 | (f["i2"] & 0x7F) << 25
+    hi = (f["i2"] >> 7) | u3 << 4
+    return lo, hi
+
+
 def test_pack_layout_is_the_documented_chunking():
     M, K = 70, 24 * 3 + 16
     nblk, T = 3, 16
     rng = np.random.default_rng(3)
     words = rng.integers(0, 1 << 48, size=(M, nblk), dtype=np.uint64)
+    words[0, 0] = 0
+    words[1, 0] = (1 << 48) - 1
     tail = rng.standard_normal((M, T)).astype(np.float16)
     blob = tt.pack_rows(words, tail, M, K)
     tiles = 2
-    for row in (0, 5, 63, 64, 69):
+    for row in (0, 1, 5, 63, 64, 69):
         tile, r = divmod(row, 64)
         for b in range(nblk):
             base = (tile * nblk + b) * 384
             lo = int(blob[base + 4 * r: base + 4 * r + 4].view(np.uint32)[0])
             hi = int(blob[base + 256 + 2 * r: base + 256 + 2 * r + 2].view(np.uint16)[0])
-            assert lo | (hi << 32) == int(words[row, b])
-    # padded rows of the last tile are zero words
+            assert (lo, hi) == _device_word(int(words[row, b]))
+    # padded rows of the last tile hold the recoded zero word
+    zlo, zhi = _device_word(0)
     base = (1 * nblk + 0) * 384
-    assert not blob[base + 4 * 6: base + 256].any()
+    assert int(blob[base + 4 * 6: base + 4 * 7].view(np.uint32)[0]) == zlo
+    assert int(blob[base + 256 + 2 * 6: base + 256 + 2 * 7].view(np.uint16)[0]) == zhi
     tail_off = (tiles * nblk * 384 + 15) // 16 * 16
+    assert tt.tail_offset(M, K) == tail_off
     assert np.array_equal(blob[tail_off:].view(np.uint16).reshape(M, T), tail.view(np.uint16))
+
+
+def test_recoding_is_one_to_one():
+    rng = np.random.default_rng(8)
+    words = rng.integers(0, 1 << 48, size=(64, 40), dtype=np.uint64)
+    blob = tt.pack_rows(words, None, 64, 960)
+    chunks = blob.reshape(40, 384)
+    lo = chunks[:, :256].view(np.uint32).astype(np.uint64)
+    hi = chunks[:, 256:].view(np.uint16).astype(np.uint64)
+    dev = (lo | hi << np.uint64(32)).T
+    assert len(set(dev.ravel().tolist())) == len(set(words.ravel().tolist()))
+    assert np.all(dev < (1 << 48))
 
 
 def test_codes_bytes_and_bits_per_weight():
@@ -124,3 +160,21 @@ def test_launch_entry_points_validate_before_touching_the_device():
     assert lib.tetra_decode(fake + 1, 4, fake, None, None) == tt.EALIGN
     assert lib.tetra_dequant(fake, None, 64, 48, fake, None) == tt.EINVAL
     assert lib.tetra_dequant(fake + 8, fake, 64, 48, fake, None) == tt.EALIGN
+
+
+def test_grouped_validation():
+    lib = tt.library()
+    fake = 0x1000
+    good = tt.Problem(fake, fake, fake, fake, 64, 48)
+    bad = tt.Problem(fake, fake, fake, fake, 64, 23)
+    arr = (tt.Problem * 17)(*([good] * 17))
+    p = ctypes.cast(arr, ctypes.c_void_p)
+    assert lib.tetra_gemv_grouped(None, 1, 1, None) == tt.EINVAL
+    assert lib.tetra_gemv_grouped(p, 0, 1, None) == tt.EINVAL
+    assert lib.tetra_gemv_grouped(p, 17, 1, None) == tt.EINVAL
+    assert lib.tetra_gemv_grouped(p, 2, 0, None) == tt.EINVAL
+    arr2 = (tt.Problem * 2)(good, bad)
+    assert lib.tetra_gemv_grouped(ctypes.cast(arr2, ctypes.c_void_p), 2, 1, None) == tt.EINVAL
+    mis = tt.Problem(fake + 8, fake, fake, fake, 64, 48)
+    arr3 = (tt.Problem * 2)(good, mis)
+    assert lib.tetra_gemv_grouped(ctypes.cast(arr3, ctypes.c_void_p), 2, 1, None) == tt.EALIGN
