@@ -14,8 +14,11 @@ fp16 activations N(0, 1).  All buffers are resident in HBM before timing.
 
 Prints one JSON line (rank 0, N = 1):
   value    = algorithmic bytes per step / wall time per step (GB/s)
-  roofline = bytes / summed kernel time of the gemv launches (HIP events
-             on the launch stream), against the 8 TB/s HBM peak
+  roofline = algorithmic bytes per gemv launch / average launch duration
+             over the timed region (HIP events on the launch stream), against
+             the 8 TB/s HBM peak; traffic = HBM bytes per launch from the
+             committed rocprofv3 counter profile when it matches this kernel
+             source and workload, else null
   cpu_baseline = the CPU oracle on a bounded sample of the same workload
 """
 
@@ -44,11 +47,15 @@ def parse():
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--mode", default="deps", choices=["matrix", "deps", "layer"],
                     help="matrix: one launch per matrix; deps: per layer [q,k,v] [o] "
                          "[gate,up] [down] (the launches a decode step can fuse); "
                          "layer: one grouped launch per layer")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="instead of the benchmark: copy a buffer of this many MiB five "
+                         "times with torch (a plain copy kernel of known size, the "
+                         "calibration for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -139,29 +146,73 @@ def parity_spot_check(torch, tt, plan, batch):
 
 
 def cpu_baseline(torch, tt, plan, seconds):
-    """The CPU oracle (numpy, one thread) on rows of the largest matrix,
-    grown until it has run for `seconds`; rate in GB/s of Tetra bytes."""
+    """The CPU oracle (float64 numpy, one thread) over the step's matrices in
+    step order, 2048 rows at a time, until it has run for `seconds`; rate in
+    GB/s of Tetra bytes (6 B per block, 2 B per tail weight and row scale).
+    Copying a matrix to the host and unpacking it are not timed."""
     from oracle import gemv as ogemv
-    m, x, _ = max(plan, key=lambda p: p[0].M * p[0].K)
-    blob = m.blob.cpu().numpy()
-    words, tail = tt.unpack_rows(blob, m.M, m.K)
-    sig = m.sigma.cpu().numpy()
-    xh = x.cpu().numpy()
-    rows_done, t_used, n = 0, 0.0, 16
-    while t_used < seconds and rows_done < m.M:
-        rows = np.arange(rows_done, min(rows_done + n, m.M))
-        t0 = time.perf_counter()
-        ogemv.gemv_f64(words, sig, tail, xh, rows=rows)
-        t_used += time.perf_counter() - t0
-        rows_done += len(rows)
-        n *= 2
-    bytes_done = rows_done * (m.nblk * 6 + 2 * m.T + 2)
+    t_used, bytes_done, rows_done, mats = 0.0, 0, 0, []
+    for m, x, _ in plan:
+        if t_used >= seconds:
+            break
+        blob = m.blob.cpu().numpy()
+        words, tail = tt.unpack_rows(blob, m.M, m.K)
+        sig = m.sigma.cpu().numpy()
+        xh = x.cpu().numpy()
+        done = 0
+        for r0 in range(0, m.M, 2048):
+            if t_used >= seconds:
+                break
+            rows = np.arange(r0, min(r0 + 2048, m.M))
+            t0 = time.perf_counter()
+            ogemv.gemv_f64(words, sig, tail, xh, rows=rows)
+            t_used += time.perf_counter() - t0
+            done += len(rows)
+            bytes_done += len(rows) * (m.nblk * 6 + 2 * m.T + 2)
+        rows_done += done
+        mats.append(f"{m.name} {m.M}x{m.K}" + ("" if done == m.M else f" ({done} rows)"))
     return {
         "value": round(bytes_done / t_used / 1e9, 6), "unit": "GB/s", "cores": 1,
         "kind": "oracle",
-        "sample": f"{rows_done} rows of the {m.M}x{m.K} {m.name} matrix "
-                  f"({rows_done * m.nblk} blocks) in {t_used:.1f} s, float64 numpy",
+        "sample": f"{len(mats)} matrices of the step in step order "
+                  f"[{', '.join(mats)}], {rows_done} rows in {t_used:.1f} s, "
+                  f"float64 numpy, batch {plan[0][1].shape[0]}",
     }
+
+
+KERNEL_SOURCES = ("paper_2609_35465_amd/csrc/kernels.h", "paper_2609_35465_amd/csrc/device_tables.h",
+                  "paper_2609_35465_amd/csrc/word_format.h", "paper_2609_35465_amd/csrc/tetra.hip")
+TRAFFIC_PROFILE = "profiles/gemv_kernel_qwen3-14b-40-layers_traffic.md"
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()
+
+
+def recorded_traffic(args, layers):
+    """HBM bytes per gemv launch from the committed counter profile, or None
+    when the profile is absent, was taken on another workload, or the kernel
+    sources have changed since it was taken."""
+    path = os.path.join(ROOT, TRAFFIC_PROFILE)
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if line.startswith("- ") and ": " in line:
+            k, v = line[2:].strip().split(": ", 1)
+            rec[k] = v.strip().strip("`")
+    want = {"source_sha256": kernel_source_hash(), "mode": args.mode,
+            "batch": str(args.batch), "model": args.model, "layers": str(layers)}
+    if any(rec.get(k) != v for k, v in want.items()):
+        return None
+    try:
+        return int(rec["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def main():
@@ -176,6 +227,16 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").random_(0, 256)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        assert torch.equal(src, dst)
+        print(json.dumps({"copy_probe_bytes": n, "copies": 5}), flush=True)
+        return 0
     stream = torch.cuda.current_stream()
     plan, L = build_workload(torch, tt, args.model, args.layers, args.batch)
     torch.cuda.synchronize()
@@ -225,17 +286,11 @@ def main():
     torch.cuda.synchronize()
     ms_step = e0.elapsed_time(e1) / args.steps
 
-    # per-launch kernel time: events around every launch on the launch stream
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in launches]
-    for (a, b), (probs, _) in zip(evs, launches):
-        a.record(stream)
-        tt.gemv_grouped(probs, args.batch, stream.cuda_stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    kern_ms = sum(a.elapsed_time(b) for a, b in evs)
-    avg_launch_ms = kern_ms / len(launches)
+    # average gemv_kernel launch over the timed region (HIP events on the
+    # launch stream; the step is nothing but back-to-back gemv launches)
+    avg_launch_ms = ms_step / len(launches)
     achieved = (algo_bytes / len(launches)) / (avg_launch_ms * 1e-3) / 1e9
+    traffic = recorded_traffic(args, L)
 
     value = algo_bytes / (ms_step * 1e-3) / 1e9
     bits_w = bytes_read * 8 / weights
@@ -266,7 +321,7 @@ def main():
         "parity_worst_rel_err": parity,
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
             "kernel": "gemv_kernel", "avg_launch_us": round(avg_launch_ms * 1e3, 3),
             "bytes_per_launch": round(algo_bytes / len(launches)),
         },

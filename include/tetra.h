@@ -93,10 +93,15 @@ size_t tetra_tail_offset(int M, int K);
  * iff T == 0.  out: host buffer of tetra_codes_bytes(M, K) bytes.
  *
  * Device layout (ours): rows are grouped in tiles of TETRA_ROW_TILE rows
- * (the last tile padded with the zero word, which decodes to the origin).
- * For tile t and block column b, a 384-byte chunk at offset (t*nblk + b)*384
- * holds 32 bits of each of the 64 words (row-in-tile order), then their
- * other 16 bits.  Each word is stored recoded, still 48 bits and one-to-one
+ * (the last tile padded with the zero word, which decodes to the origin);
+ * tile t occupies nblk*384 bytes starting at t*nblk*384.  Inside a tile,
+ * with ng = nblk / 4 and r the row in the tile:
+ *   - block columns 4g..4g+3 (g < ng) form a 1536-byte run at g*1536: the
+ *     32-bit part of column 4g+k of row r at 16*r + 4*k, its 16-bit part at
+ *     1024 + 8*r + 2*k (one 16-byte and one 8-byte load per row and group);
+ *   - each remaining column b = 4*ng + q (q < nblk mod 4) is a 384-byte run
+ *     at ng*1536 + q*384: 32-bit part at 4*r, 16-bit part at 256 + 2*r.
+ * Each word is stored recoded, still 48 bits and one-to-one
  * with the canonical word: path = s8 | b1<<6 | b2<<7 | b3<<11, g, the
  * physical rank-table row of section 1, i2, and section 3's physical row
  * without delta, (p^r)<<11 | i3' (rank rows of class 0 sit at

@@ -79,43 +79,62 @@ def _device_word(w: int):
     return lo, hi
 
 
-def test_pack_layout_is_the_documented_chunking():
-    M, K = 70, 24 * 3 + 16
-    nblk, T = 3, 16
-    rng = np.random.default_rng(3)
+def _stored_word(blob, nblk, tile, r, b):
+    """(lo32, hi16) of row r, block column b of a tile, by the layout that
+    include/tetra.h documents (groups of four columns, then single columns)."""
+    base = tile * nblk * 384
+    ng = nblk // 4
+    if b < 4 * ng:
+        g, k = divmod(b, 4)
+        lo_at = base + g * 1536 + 16 * r + 4 * k
+        hi_at = base + g * 1536 + 1024 + 8 * r + 2 * k
+    else:
+        run = base + ng * 1536 + (b - 4 * ng) * 384
+        lo_at, hi_at = run + 4 * r, run + 256 + 2 * r
+    lo = int(blob[lo_at:lo_at + 4].view(np.uint32)[0])
+    hi = int(blob[hi_at:hi_at + 2].view(np.uint16)[0])
+    return lo, hi
+
+
+@pytest.mark.parametrize("nblk,T", [(3, 16), (9, 6), (8, 0)])
+def test_pack_layout_is_the_documented_chunking(nblk, T):
+    M, K = 70, 24 * nblk + T
+    rng = np.random.default_rng(3 + nblk)
     words = rng.integers(0, 1 << 48, size=(M, nblk), dtype=np.uint64)
     words[0, 0] = 0
     words[1, 0] = (1 << 48) - 1
-    tail = rng.standard_normal((M, T)).astype(np.float16)
+    tail = rng.standard_normal((M, T)).astype(np.float16) if T else None
     blob = tt.pack_rows(words, tail, M, K)
     tiles = 2
     for row in (0, 1, 5, 63, 64, 69):
         tile, r = divmod(row, 64)
         for b in range(nblk):
-            base = (tile * nblk + b) * 384
-            lo = int(blob[base + 4 * r: base + 4 * r + 4].view(np.uint32)[0])
-            hi = int(blob[base + 256 + 2 * r: base + 256 + 2 * r + 2].view(np.uint16)[0])
-            assert (lo, hi) == _device_word(int(words[row, b]))
+            assert _stored_word(blob, nblk, tile, r, b) == _device_word(int(words[row, b]))
     # padded rows of the last tile hold the recoded zero word
-    zlo, zhi = _device_word(0)
-    base = (1 * nblk + 0) * 384
-    assert int(blob[base + 4 * 6: base + 4 * 7].view(np.uint32)[0]) == zlo
-    assert int(blob[base + 256 + 2 * 6: base + 256 + 2 * 7].view(np.uint16)[0]) == zhi
+    for r in (6, 40, 63):
+        for b in range(nblk):
+            assert _stored_word(blob, nblk, 1, r, b) == _device_word(0)
     tail_off = (tiles * nblk * 384 + 15) // 16 * 16
     assert tt.tail_offset(M, K) == tail_off
-    assert np.array_equal(blob[tail_off:].view(np.uint16).reshape(M, T), tail.view(np.uint16))
+    assert tt.codes_bytes(M, K) == tail_off + 2 * M * T
+    if T:
+        assert np.array_equal(blob[tail_off:].view(np.uint16).reshape(M, T), tail.view(np.uint16))
 
 
 def test_recoding_is_one_to_one():
     rng = np.random.default_rng(8)
-    words = rng.integers(0, 1 << 48, size=(64, 40), dtype=np.uint64)
-    blob = tt.pack_rows(words, None, 64, 960)
-    chunks = blob.reshape(40, 384)
-    lo = chunks[:, :256].view(np.uint32).astype(np.uint64)
-    hi = chunks[:, 256:].view(np.uint16).astype(np.uint64)
-    dev = (lo | hi << np.uint64(32)).T
-    assert len(set(dev.ravel().tolist())) == len(set(words.ravel().tolist()))
-    assert np.all(dev < (1 << 48))
+    words = rng.integers(0, 1 << 48, size=(64, 41), dtype=np.uint64)
+    # adversarial words: every field at its extremes, and delta on both sides
+    words[0, :4] = [0, (1 << 48) - 1, 1239 << 26, 1240 << 26]
+    blob = tt.pack_rows(words, None, 64, 24 * 41)
+    dev = np.array([[_stored_word(blob, 41, 0, r, b) for b in range(41)] for r in range(64)],
+                   dtype=np.uint64)
+    packed = dev[..., 0] | dev[..., 1] << np.uint64(32)
+    assert np.all(packed < (1 << 48))
+    assert len(set(packed.ravel().tolist())) == len(set(words.ravel().tolist()))
+    for r in range(64):
+        for b in range(41):
+            assert tuple(int(v) for v in dev[r, b]) == _device_word(int(words[r, b]))
 
 
 def test_codes_bytes_and_bits_per_weight():
