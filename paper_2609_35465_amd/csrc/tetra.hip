@@ -20,7 +20,6 @@ using tetra_dev::kChunk;
 using tetra_dev::kTile;
 
 constexpr int kMaxDevices = 64;
-constexpr size_t kMaxLds = 160 * 1024;     // LDS per workgroup on gfx950
 
 std::mutex g_init_mu;
 bool g_init_done[kMaxDevices];
@@ -48,17 +47,6 @@ int ensure_tables(int* dev_out) {
     if (hipMemcpyToSymbol(HIP_SYMBOL(tetra_dev::g_packed), pk, sizeof(*pk), 0, hipMemcpyHostToDevice) !=
         hipSuccess)
         return TETRA_EDEVICE;
-    // kernels staging the packed tables need more than the default 64 KiB
-    const void* big[] = {
-        reinterpret_cast<const void*>(tetra_dev::dequant_kernel),
-        reinterpret_cast<const void*>(tetra_dev::gemv_kernel<1>), reinterpret_cast<const void*>(tetra_dev::gemv_kernel<2>),
-        reinterpret_cast<const void*>(tetra_dev::gemv_kernel<3>), reinterpret_cast<const void*>(tetra_dev::gemv_kernel<4>),
-        reinterpret_cast<const void*>(tetra_dev::gemv_kernel<5>), reinterpret_cast<const void*>(tetra_dev::gemv_kernel<6>),
-        reinterpret_cast<const void*>(tetra_dev::gemv_kernel<7>), reinterpret_cast<const void*>(tetra_dev::gemv_kernel<8>)};
-    for (const void* f : big)
-        if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kMaxLds)) !=
-            hipSuccess)
-            return TETRA_EDEVICE;
     g_init_done[dev] = true;
     return TETRA_OK;
 }
@@ -121,7 +109,7 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t s
         P.T = s.T;
         P.tail_off = s.tail_off;
         P.tiles = s.tiles;
-        const int items = s.nblk / 4 + s.nblk % 4;
+        const int items = s.nblk / 4 + (s.nblk % 4 > 0 ? 1 : 0);
         P.round_tiles = tetra_dev::round_tiles_for(items, batch);
         P.round_begin = static_cast<int>(rounds);
         rounds += (s.tiles + P.round_tiles - 1) / P.round_tiles;
@@ -132,12 +120,11 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t s
     int dev;
     if (int st = ensure_tables(&dev)) return st;
     const int cus = num_cus(dev);
-    const int grid = std::min(grp.total_rounds, cus);
-    const size_t lds = tetra_dev::gemv_lds_bytes(batch);
+    const int grid = std::min(grp.total_rounds, cus * tetra_dev::gemv_wgs_per_cu(batch));
 #define TETRA_LAUNCH(B)                                                                           \
     case B:                                                                                       \
         hipLaunchKernelGGL(tetra_dev::gemv_kernel<B>, dim3(grid), dim3(tetra_dev::kGemvThreads), \
-                           lds, stream, grp);                                                     \
+                           0, stream, grp);                                                     \
         break;
     switch (batch) {
         TETRA_LAUNCH(1) TETRA_LAUNCH(2) TETRA_LAUNCH(3) TETRA_LAUNCH(4)
@@ -278,7 +265,7 @@ int tetra_dequant(const void* codes, const uint16_t* row_scales, int M, int K, f
     const size_t units = static_cast<size_t>(s.tiles) * s.nblk;
     const size_t blocks = std::min<size_t>((units + 3) / 4, static_cast<size_t>(num_cus(dev)) * 2);
     hipLaunchKernelGGL(tetra_dev::dequant_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256),
-                       tetra_dev::kPackedTableBytes, stream,
+                       0, stream,
                        static_cast<const uint8_t*>(codes), row_scales, M, K, s.nblk, s.T,
                        s.tail_off, w_out);
     return launch_status();
