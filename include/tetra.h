@@ -23,9 +23,15 @@
  * Memory: all buffers are owned by the caller.  "host" arguments are plain
  * host pointers; "device" arguments are device pointers on the current HIP
  * device (for example from hipMalloc or torch.empty(..., device="cuda")).
- * The library owns only its constant decoder tables, uploaded once per
- * device on first use (thread-safe).  Launching calls are asynchronous on
- * the given stream, never synchronise and never allocate.
+ * The library owns its constant decoder tables and one GEMV workspace per
+ * device (a counter and two partial sums per workgroup, about 3 MB on a
+ * 256-CU part), both set up on the first call on the device (thread-safe;
+ * make that first call outside stream capture).  After that, launching calls
+ * are asynchronous on the given stream, never synchronise and never
+ * allocate.  The workspace is shared by the GEMV calls of a device: GEMV
+ * calls on one device must not overlap in time (issue them on one stream,
+ * or order the streams); the counters return to zero at the end of every
+ * launch.
  *
  * Errors: every call validates its arguments before any launch and returns
  * a tetra_status.  TETRA_EDEVICE reports a HIP error seen at launch time;
@@ -122,7 +128,11 @@ int tetra_unpack_rows(const void* codes, size_t codes_bytes, int M, int K,
                       uint64_t* words, uint16_t* tail);
 
 /*
- * Fused decode and matrix-vector product (Sec. 5.1, Eq. 2):
+ * Fused decode and matrix-vector product (Sec. 5.1, Eq. 2).  The blocks are
+ * split evenly over the waves of the launch; pieces of a row tile held by
+ * several waves are added in a fixed order, so y is deterministic and the
+ * row for activation b of a batch-B call equals the batch-1 result for x_b
+ * bit for bit (a grouped call may round differently from single calls):
  *   y[b][row] = sigma_row * sum_blk s_blk * sum_j y_j x[b][24*blk + j]
  *               + sum_t tail[row][t] * x[b][24*nblk + t]
  * with s_blk = gain[g] * (1/sqrt(16 m)) in f32 and f32 accumulation.

@@ -11,8 +11,9 @@ namespace tetra_dev {
 
 constexpr int kTile = 64;                 // rows per code tile = lanes per wave
 constexpr int kChunk = kTile * 6;         // bytes per (tile, block column) chunk
-constexpr int kGemvWaves = 16;
+constexpr int kGemvWaves = 8;                  // waves per GEMV workgroup
 constexpr int kGemvThreads = kGemvWaves * 64;
+constexpr int kGemvGroupsPerCU = 3;            // at batch 1: 3 x 54.5 KB of LDS, 6 waves per SIMD
 constexpr int kMaxGroup = 16;
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
@@ -157,10 +158,32 @@ __device__ __forceinline__ uint32_t block_values(const BlockFetch& f, uint32_t y
     return (__builtin_bit_cast(uint32_t, sq) >> 2) & 0x7FFu;
 }
 
+// Decoder tables into LDS: all loads first, then all stores, so that a
+// workgroup pays one memory round trip (NT: threads of the workgroup).
+template <int NT>
+struct TableStage {
+    static constexpr int kN = static_cast<int>(kPackedTableBytes / 16);
+    static constexpr int kPer = (kN + NT - 1) / NT;
+    uint4 v[kPer];
+    __device__ __forceinline__ void load() {
+        const uint4* src = reinterpret_cast<const uint4*>(&g_packed);
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) v[k] = src[min(static_cast<int>(threadIdx.x) + k * NT, kN - 1)];
+    }
+    __device__ __forceinline__ void store(uint4* dst) const {
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int i = static_cast<int>(threadIdx.x) + k * NT;
+            if (i < kN) dst[i] = v[k];
+        }
+    }
+};
+
+template <int NT>
 __device__ __forceinline__ void stage_packed_tables(uint4* dst) {
-    const uint4* src = reinterpret_cast<const uint4*>(&g_packed);
-    for (int i = threadIdx.x; i < static_cast<int>(kPackedTableBytes / 16); i += blockDim.x)
-        dst[i] = src[i];
+    TableStage<NT> ts;
+    ts.load();
+    ts.store(dst);
 }
 
 __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict__ codes,
@@ -168,7 +191,7 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
                                                       int K, int nblk, int T, size_t tail_off,
                                                       float* __restrict__ w_out) {
     __shared__ uint4 s_tab[kPackedTableBytes / 16];
-    stage_packed_tables(s_tab);
+    stage_packed_tables<256>(s_tab);
     __syncthreads();
     lds_bytes* L = (lds_bytes*)(s_tab);
     const int lane = threadIdx.x & 63;
@@ -207,55 +230,86 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
 
 // ------------------------------------------------------------------ GEMV
 //
-// One lane per output row (64-row tiles).  A persistent workgroup of 16
-// waves works in rounds; a round is 1-4 consecutive tiles of one matrix
-// (more tiles for short rows, so that every wave gets about six items).
-// The round's items -- groups of four block columns, then one item with
-// the nblk mod 4 remaining columns, tile by tile -- are dealt round-robin
-// (item i to wave i mod 16).  Each wave runs its blocks as a pipeline: the
-// table reads and activation loads of the next block are issued before the
-// current block's arithmetic, the current block's scale read is consumed
-// one block later, and the code words of the next item are loaded one item
-// ahead, so a wave waits at most once per block.  Partial sums are combined
-// in LDS in a fixed order, so the result does not depend on timing or on
-// the batch size.  Rounds go to workgroups in serpentine order over
-// matrices sorted by decreasing row length (done on the host).  The
-// activation pairs of a block column are identical for all lanes and come
-// through the scalar unit as SGPR operands of v_dot2_f32_f16.
-
-constexpr int kMaxRoundTiles = 4;
+// One lane per output row (64-row tiles).  The blocks of all matrices of a
+// launch form one sequence (matrix by matrix, tile by tile, block column by
+// block column), and wave w of the W waves of the launch takes the
+// contiguous range [floor(w Tot / W), floor((w+1) Tot / W)): every wave gets
+// the same number of blocks to within one, whatever the shapes.  A range
+// covers whole tiles and at most two pieces of tiles.  A whole tile is
+// finished by its wave (row scale, unquantised tail, store of y); the waves
+// holding pieces of one tile store their partial sums to the workspace and
+// count themselves in on the tile's counter, and the last one to arrive adds
+// the pieces in wave order, finishes the tile and resets the counter.  The
+// ranges depend only on the shapes and W, never on timing or on the batch,
+// so the result is deterministic and row b of a batch-B product is the
+// batch-1 product of x_b bit for bit.
+//
+// Inside its range a wave runs the blocks as a pipeline: the table reads and
+// activation loads of the next block are issued before the current block's
+// arithmetic, the current block's scale read is consumed one block later,
+// and the code words of the next group of four columns are loaded one group
+// ahead, so a wave waits at most once per block.  The activation pairs of a
+// block column are the same for all lanes and come through the scalar unit
+// as SGPR operands of v_dot2_f32_f16.
 
 struct GemvProblem {
     const uint8_t* codes;
     const uint16_t* sigma;
     const uint16_t* x;
     float* y;
-    int M, K, nblk, T;
     unsigned long long tail_off;
-    int tiles, round_tiles, round_begin, pad;
+    uint32_t blk_base;             // index of the matrix's first block in the launch sequence
+    int M, K, nblk, T;
+    int tiles, ng, rem;
 };
 
 struct GemvGroup {
     GemvProblem prob[kMaxGroup];
-    int n, total_rounds, pad0, pad1;
+    double inv_total, inv_waves;   // 1 / total, 1 / waves
+    uint32_t total;                // blocks in the launch sequence (< 2^31)
+    uint32_t* counters;            // [W / 16], zero between launches
+    float* partials;               // [W / 16][2][B][64]
+    int n, waves;
 };
 
-// reduction slots (tile x batch row) per wave
-__host__ __device__ constexpr int red_slots(int B) { return B <= 4 ? 4 : 8; }
-
-// workgroups that fit on one CU (LDS bound)
-inline int gemv_wgs_per_cu(int B) { return B <= 2 ? 2 : 1; }
-
-// tiles per round for a matrix with `items` items per tile (B: batch)
-inline int round_tiles_for(int items, int B) {
-    int t = 1;
-    while (t < kMaxRoundTiles && 2 * t * B <= red_slots(B) && t * items < 6 * kGemvWaves) t *= 2;
-    return t;
+// wave count of a launch: three 512-thread workgroups per CU, fewer when
+// there are fewer blocks than waves (every wave's range must be non-empty);
+// independent of the batch size
+inline int gemv_waves(uint32_t total, int cus) {
+    const uint32_t cap = static_cast<uint32_t>(cus) * kGemvGroupsPerCU * kGemvWaves;
+    return static_cast<int>(total < cap ? total : cap);
 }
 
+// workspace bytes for G workgroups at batch B: a counter and two partial
+// sums per workgroup
+inline size_t gemv_workspace_bytes(int G, int B) {
+    return static_cast<size_t>(G) * sizeof(uint32_t) + static_cast<size_t>(G) * 2 * B * 64 * sizeof(float);
+}
 
-// code words of one item: up to four blocks; the 16-bit part of block k is
-// in hi.x (k = 0, 1) or hi.y (k = 2, 3), low half for even k
+// floor(n / d) for n < 2^53, from a reciprocal of d computed on the host
+// (exact: the estimate is corrected by one in either direction)
+__device__ __forceinline__ uint32_t div_exact(unsigned long long n, uint32_t d, double inv_d) {
+    uint32_t q = static_cast<uint32_t>(static_cast<double>(n) * inv_d);
+    const unsigned long long qd = static_cast<unsigned long long>(q) * d;
+    if (qd > n) --q;
+    else if (qd + d <= n) ++q;
+    return q;
+}
+
+__device__ __forceinline__ uint32_t range_begin(int w, const GemvGroup& grp) {
+    return div_exact(static_cast<unsigned long long>(grp.total) * static_cast<uint32_t>(w),
+                     static_cast<uint32_t>(grp.waves), grp.inv_waves);
+}
+
+// the wave whose range holds block i: floor(((i + 1) W - 1) / total)
+__device__ __forceinline__ int wave_of(uint32_t i, const GemvGroup& grp) {
+    return static_cast<int>(div_exact(static_cast<unsigned long long>(i + 1) * static_cast<uint32_t>(grp.waves) - 1,
+                                      grp.total, grp.inv_total));
+}
+
+// code words of one item (a group of four block columns, or the nblk mod 4
+// single columns of a tile): the 16-bit part of block k is in hi.x (k = 0,
+// 1) or hi.y (k = 2, 3), low half for even k
 struct ItemWords {
     uint4 lo;
     uint2 hi;
@@ -267,17 +321,16 @@ __device__ __forceinline__ void block_word(const ItemWords& w, uint32_t& lo, uin
     hi = K == 0 ? w.hi.x : K == 1 ? w.hi.x >> 16 : K == 2 ? w.hi.y : w.hi.y >> 16;
 }
 
-// per-wave pipeline state: the staged block, its activation pairs (B <= 2),
-// and the previous block, whose scale read is still in flight
+// per-wave pipeline state: the staged block and its activation pairs (batch
+// 1), the previous block (scale read in flight, dot products), and the
+// running sums of the current piece of a tile
 template <int B>
 struct Pipe {
     static constexpr bool kStageX = B == 1;
     BlockFetch cur;
     uint32_t x[kStageX ? B : 1][12];
-    float ps;              // scale of the previous block
-    float pdt[B];          // its dot products
-    int pend_t;            // its tile in the round (-1: none)
-    int acc_t;             // tile of acc
+    float ps;              // zero before the first block, so that adding the
+    float pdt[B];          // "previous block" is a no-op there
     float acc[B];
 };
 
@@ -292,214 +345,350 @@ __device__ __forceinline__ void load_x(uint32_t (&x)[Pipe<B>::kStageX ? B : 1][1
     }
 }
 
-// adds the previous block into acc, first storing acc when it ends a tile
 template <int B>
-__device__ __forceinline__ void finish_pending(Pipe<B>& st, float* red) {
-    if (st.pend_t >= 0) {
-        if (st.pend_t != st.acc_t) {
+__device__ __forceinline__ void finish_pending(Pipe<B>& st) {
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) st.acc[bb] = fmaf(st.ps, st.pdt[bb], st.acc[bb]);
+}
+
+// Blocks kb..ke-1 of one item (block k is column col0 + k), each one staging
+// the next: block k+1 of this item, or block 0 of the next item (words nw,
+// column ncol0; a repeat of this item at the end of a piece).  Full: the
+// whole group of four.
+template <int B, bool Full>
+__device__ __forceinline__ void run_item(Pipe<B>& st, const ItemWords& cw, const ItemWords& nw, int col0,
+                                         int ncol0, int kb, int ke, lds_bytes* L, const_u32* xc, int kp) {
+#pragma unroll
+    for (int k = 0; k < tetra::kGroupCols; ++k) {
+        if (Full || (k >= kb && k < ke)) {
+            uint32_t lo, hi;
+            int ncol;
+            BlockFetch nxt;
+            if (k + 1 < tetra::kGroupCols && (Full || k + 1 < ke)) {
+                if (k == 0) block_word<1>(cw, lo, hi);
+                else if (k == 1) block_word<2>(cw, lo, hi);
+                else block_word<3>(cw, lo, hi);
+                ncol = col0 + k + 1;
+            } else {
+                block_word<0>(nw, lo, hi);
+                ncol = ncol0;
+            }
+            nxt = fetch_block(lo, hi, L);
+            uint32_t xn[Pipe<B>::kStageX ? B : 1][12];
+            load_x<B>(xn, xc, kp, ncol);
+            __builtin_amdgcn_sched_barrier(0);
+            // values and norm of the current block (its reads were waited for one block ago)
+            uint32_t y[12];
+            const uint32_t sa = block_values(st.cur, y);
+            __builtin_amdgcn_sched_barrier(0);
+            // one wait per block: the next block's reads and the previous block's scale
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            finish_pending<B>(st);
+            st.ps = *(lds_f32*)(L + kScaleOff + sa);
 #pragma unroll
             for (int bb = 0; bb < B; ++bb) {
-                red[(st.acc_t * B + bb) * 64] = st.acc[bb];
-                st.acc[bb] = 0.f;
-            }
-            st.acc_t = st.pend_t;
-        }
+                float dt = 0.f;
 #pragma unroll
-        for (int bb = 0; bb < B; ++bb) st.acc[bb] = fmaf(st.ps, st.pdt[bb], st.acc[bb]);
+                for (int q = 0; q < 12; ++q) {
+                    uint32_t xv;
+                    if constexpr (Pipe<B>::kStageX) xv = st.x[bb][q];
+                    else xv = xc[bb * kp + 12 * (col0 + k) + q];
+                    dt = dot2(y[q], xv, dt);
+                }
+                asm volatile("" : : "v"(dt));      // computed here, not sunk into the next block
+                st.pdt[bb] = dt;
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            st.cur = nxt;
+            if constexpr (Pipe<B>::kStageX) {
+#pragma unroll
+                for (int bb = 0; bb < B; ++bb)
+#pragma unroll
+                    for (int q = 0; q < 12; ++q) st.x[bb][q] = xn[bb][q];
+            }
+        }
     }
 }
 
-// The NB blocks of one item (columns col0..col0+NB-1 of tile t), each one
-// staging the next: block k+1 of this item, or block 0 of the next item
-// (words nw, column ncol0; a repeat of this item when there is none).
-template <int B, int NB>
-__device__ __forceinline__ void run_item(Pipe<B>& st, const ItemWords& cw, const ItemWords& nw, int col0,
-                                         int ncol0, int t, lds_bytes* L, const_u32* xc, int kp,
-                                         float* red) {
-#pragma unroll
-    for (int k = 0; k < NB; ++k) {
-        // issue the reads of the next block: block k+1 of this item or block 0 of the next
-        uint32_t lo, hi;
-        if (k + 1 < NB) {
-            if (k == 0) block_word<1>(cw, lo, hi);
-            else if (k == 1) block_word<2>(cw, lo, hi);
-            else block_word<3>(cw, lo, hi);
-        } else {
-            block_word<0>(nw, lo, hi);
+__device__ __forceinline__ ItemWords load_item(const uint8_t* tb, int j, int ng, int rem, int lane) {
+    ItemWords w;
+    if (j < ng) {
+        const uint8_t* gp = tb + static_cast<size_t>(j) * tetra::kGroupBytes;
+        w.lo = *reinterpret_cast<const uint4*>(gp + 16 * lane);
+        w.hi = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * lane);
+    } else {
+        // the nblk mod 4 single columns, 384-byte runs
+        const uint8_t* sp = tb + static_cast<size_t>(ng) * tetra::kGroupBytes;
+        w.lo = make_uint4(0, 0, 0, 0);
+        w.lo.x = *reinterpret_cast<const uint32_t*>(sp + 4 * lane);
+        uint32_t h0 = *reinterpret_cast<const uint16_t*>(sp + 256 + 2 * lane), h1 = 0, h2 = 0;
+        if (rem > 1) {
+            w.lo.y = *reinterpret_cast<const uint32_t*>(sp + kChunk + 4 * lane);
+            h1 = *reinterpret_cast<const uint16_t*>(sp + kChunk + 256 + 2 * lane);
         }
-        const int ncol = k + 1 < NB ? col0 + k + 1 : ncol0;
-        const BlockFetch nxt = fetch_block(lo, hi, L);
-        uint32_t xn[Pipe<B>::kStageX ? B : 1][12];
-        load_x<B>(xn, xc, kp, ncol);
-        __builtin_amdgcn_sched_barrier(0);
-        // values and norm of the current block (its reads were waited for one block ago)
-        uint32_t y[12];
-        const uint32_t sa = block_values(st.cur, y);
-        __builtin_amdgcn_sched_barrier(0);
-        // one wait per block: the next block's reads and the previous block's scale
-        __builtin_amdgcn_s_waitcnt(0xC07F);
-        finish_pending<B>(st, red);
-        st.ps = *(lds_f32*)(L + kScaleOff + sa);
-#pragma unroll
-        for (int bb = 0; bb < B; ++bb) {
-            float dt = 0.f;
-#pragma unroll
-            for (int q = 0; q < 12; ++q) {
-                uint32_t xv;
-                if constexpr (Pipe<B>::kStageX) xv = st.x[bb][q];
-                else xv = xc[bb * kp + 12 * (col0 + k) + q];
-                dt = dot2(y[q], xv, dt);
-            }
-            asm volatile("" : : "v"(dt));      // computed here, not sunk into the next block
-            st.pdt[bb] = dt;
+        if (rem > 2) {
+            w.lo.z = *reinterpret_cast<const uint32_t*>(sp + 2 * kChunk + 4 * lane);
+            h2 = *reinterpret_cast<const uint16_t*>(sp + 2 * kChunk + 256 + 2 * lane);
         }
-        st.pend_t = t;
-        __builtin_amdgcn_sched_barrier(0);
-        st.cur = nxt;
-        if constexpr (Pipe<B>::kStageX) {
-#pragma unroll
-            for (int bb = 0; bb < B; ++bb)
-#pragma unroll
-                for (int q = 0; q < 12; ++q) st.x[bb][q] = xn[bb][q];
-        }
+        w.hi = make_uint2(h0 | h1 << 16, h2);
     }
+    return w;
+}
+
+// A piece of a tile: block columns c0..c1-1 of tile t.  begin_piece issues
+// the loads of its first two items, so that they can be in flight while the
+// workgroup stages its tables; run_piece sums the piece for the wave's 64 rows.
+struct Piece {
+    ItemWords cw, nw;
+    int t, c0, c1, j, j1;
+};
+
+__device__ __forceinline__ Piece begin_piece(const GemvProblem& P, int t, int c0, int c1, int lane) {
+    Piece pc;
+    pc.t = t;
+    pc.c0 = c0;
+    pc.c1 = c1;
+    pc.j = min(c0 >> 2, P.ng);
+    pc.j1 = min((c1 - 1) >> 2, P.ng);
+    const uint8_t* tb = P.codes + static_cast<size_t>(t) * P.nblk * kChunk;
+    pc.cw = load_item(tb, pc.j, P.ng, P.rem, lane);
+    pc.nw = load_item(tb, min(pc.j + 1, pc.j1), P.ng, P.rem, lane);
+    return pc;
+}
+
+// blocks of item j whose words are in cw (next item's words in nw)
+template <int B>
+__device__ __forceinline__ void run_one_item(Pipe<B>& st, const GemvProblem& P, const Piece& pc, int j, int kb,
+                                             const ItemWords& cw, const ItemWords& nw, lds_bytes* L,
+                                             const_u32* xc, int kp) {
+    const int ke = __builtin_amdgcn_readfirstlane(j == pc.j1 ? pc.c1 - 4 * j : (j < P.ng ? tetra::kGroupCols : P.rem));
+    const int col0 = __builtin_amdgcn_readfirstlane(4 * j);
+    const int ncol0 = __builtin_amdgcn_readfirstlane(4 * min(j + 1, pc.j1));
+    if (kb == 0 && ke == tetra::kGroupCols)
+        run_item<B, true>(st, cw, nw, col0, ncol0, 0, tetra::kGroupCols, L, xc, kp);
+    else
+        run_item<B, false>(st, cw, nw, col0, ncol0, kb, ke, L, xc, kp);
+}
+
+// The items alternate between two sets of word registers, so that the loads
+// of the item after next go straight into the registers just freed.
+template <int B>
+__device__ __forceinline__ void run_piece(const GemvProblem& P, Piece& pc, lds_bytes* L, float (&out)[B]) {
+    const int ng = P.ng;
+    const int lane = threadIdx.x & 63;
+    const uint8_t* tb = P.codes + static_cast<size_t>(pc.t) * P.nblk * kChunk;
+    const_u32* xc = (const_u32*)(P.x);
+    const int kp = P.K >> 1;
+    const int j1 = pc.j1;
+    int j = pc.j;
+    int kb = pc.c0 - 4 * j;
+    Pipe<B> st;
+    {
+        uint32_t lo, hi;
+        if (kb == 0) block_word<0>(pc.cw, lo, hi);
+        else if (kb == 1) block_word<1>(pc.cw, lo, hi);
+        else if (kb == 2) block_word<2>(pc.cw, lo, hi);
+        else block_word<3>(pc.cw, lo, hi);
+        st.cur = fetch_block(lo, hi, L);
+        load_x<B>(st.x, xc, kp, pc.c0);
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+    }
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) st.acc[bb] = st.pdt[bb] = 0.f;
+    st.ps = 0.f;
+    ItemWords wa = pc.cw, wb = pc.nw;
+    for (;;) {
+        run_one_item<B>(st, P, pc, j, kb, wa, wb, L, xc, kp);
+        if (j == j1) break;
+        ++j;
+        kb = 0;
+        wa = load_item(tb, min(j + 1, j1), ng, P.rem, lane);
+        run_one_item<B>(st, P, pc, j, 0, wb, wa, L, xc, kp);
+        if (j == j1) break;
+        ++j;
+        wb = load_item(tb, min(j + 1, j1), ng, P.rem, lane);
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    finish_pending<B>(st);
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) out[bb] = st.acc[bb];
+}
+
+// y of a tile's rows: sigma_row * sum + unquantised tail (T = K mod 24 is
+// even, so the tail is at most 11 fp16 pairs).  load_rows issues the loads,
+// store_rows does the arithmetic and the stores, so that the loads can be in
+// flight while the sums are being combined.
+struct RowTail {
+    uint32_t tv[11];
+    float sg;
+};
+
+__device__ __forceinline__ RowTail load_rows(const GemvProblem& P, int t, int lane) {
+    RowTail r;
+    const int row = min(t * kTile + lane, P.M - 1);
+    const uint32_t* tl =
+        reinterpret_cast<const uint32_t*>(P.codes + P.tail_off) + static_cast<size_t>(row) * (P.T >> 1);
+    r.sg = f16(P.sigma[row]);
+#pragma unroll
+    for (int q = 0; q < 11; ++q) r.tv[q] = 2 * q < P.T ? tl[q] : 0u;
+    return r;
 }
 
 template <int B>
-__global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(B <= 2 ? 8 : 4)))
+__device__ __forceinline__ void store_rows(const GemvProblem& P, int t, int lane, const float (&tot)[B],
+                                           const RowTail& r) {
+    const int row = t * kTile + lane;
+    if (row >= P.M) return;
+    const_u32* xc = (const_u32*)(P.x);
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) {
+        const int x0 = bb * (P.K >> 1) + 12 * P.nblk;     // first tail pair of x_b
+        float ts = 0.f;
+#pragma unroll
+        for (int q = 0; q < 11; ++q)
+            if (2 * q < P.T) ts = dot2(r.tv[q], xc[x0 + q], ts);
+        P.y[static_cast<size_t>(bb) * P.M + row] = fmaf(r.sg, tot[bb], ts);
+    }
+}
+
+// Pieces of a tile are combined in two levels: the waves of one workgroup
+// that hold pieces of the tile add them in LDS (the last of them to arrive,
+// in wave order), and when the tile reaches into other workgroups each
+// workgroup's sum goes to the workspace, where the last workgroup to arrive
+// adds them in workgroup order.
+template <int B>
+__global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(B == 1 ? 6 : B <= 4 ? 4 : 2)))
 void gemv_kernel(const GemvGroup grp) {
-    constexpr int S = red_slots(B);
     __shared__ uint4 s_tab[kPackedTableBytes / 16];
-    __shared__ float s_red[kGemvWaves * S * 64];     // [wave][slot][64]
-    stage_packed_tables(s_tab);
+    __shared__ float s_piece[kGemvWaves * 2 * B * 64];   // [wave][first/last piece][B][64]
+    __shared__ uint32_t s_cnt[2 * kGemvWaves];
+    if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
     lds_bytes* L = (lds_bytes*)(s_tab);
-
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
-    const int G = gridDim.x;
+    const int W = grp.waves;
+    const int wid = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    const int g = static_cast<int>(blockIdx.x);
+    const int w0 = g * kGemvWaves;
+    const int w = w0 + wid;
+    const int wlast = min(w0 + kGemvWaves, W) - 1;
+    stage_packed_tables<kGemvThreads>(s_tab);
     __syncthreads();
-
-    for (int kr = 0;; ++kr) {
-        const int r = kr * G + ((kr & 1) ? G - 1 - static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x));
-        if (r >= grp.total_rounds) break;                  // uniform over the workgroup
-        int pi = 0;
-        while (pi + 1 < grp.n && r >= grp.prob[pi + 1].round_begin) ++pi;
-        const GemvProblem& P = grp.prob[pi];
-        const int tile0 = (r - P.round_begin) * P.round_tiles;
-        const int ntr = min(P.round_tiles, P.tiles - tile0);
-        const int nblk = P.nblk;
-        const int ng = nblk / tetra::kGroupCols;
-        const int rem = nblk - ng * tetra::kGroupCols;
-        const int per_tile = ng + (rem > 0 ? 1 : 0);
-        const size_t tile_bytes = static_cast<size_t>(nblk) * kChunk;
-        const uint8_t* tb0 = P.codes + static_cast<size_t>(tile0) * tile_bytes;
-        const_u32* xc = (const_u32*)(P.x);
-        const int kp = P.K >> 1;
-        float* red = s_red + wave * S * 64 + lane;
-
-        // this wave's slots start at zero: tiles it gets no item of stay zero
+    if (w >= W) return;
+    uint32_t i = __builtin_amdgcn_readfirstlane(range_begin(w, grp));
+    const uint32_t end = __builtin_amdgcn_readfirstlane(range_begin(w + 1, grp));
+    int p = 0;
+    while (p + 1 < grp.n && i >= grp.prob[p + 1].blk_base) ++p;
+    const uint32_t rel = i - grp.prob[p].blk_base;
+    int t = __builtin_amdgcn_readfirstlane(static_cast<int>(rel / static_cast<uint32_t>(grp.prob[p].nblk)));
+    int c = __builtin_amdgcn_readfirstlane(static_cast<int>(rel - static_cast<uint32_t>(t) * grp.prob[p].nblk));
+    int c1;
+    {
+        const uint32_t left = end - i;
+        c1 = left < static_cast<uint32_t>(grp.prob[p].nblk - c) ? c + static_cast<int>(left) : grp.prob[p].nblk;
+    }
+    Piece pc = begin_piece(grp.prob[p], t, c, c1, lane);
+    bool first = true;
+    for (;;) {
+        const GemvProblem& P = grp.prob[p];
+        float sum[B];
+        run_piece<B>(P, pc, L, sum);
+        if (c == 0 && c1 == P.nblk) {
+            const RowTail rt = load_rows(P, t, lane);
+            store_rows<B>(P, t, lane, sum, rt);
+        } else {
+            const uint32_t t0 = P.blk_base + static_cast<uint32_t>(t) * P.nblk;
+            const int wa = __builtin_amdgcn_readfirstlane(wave_of(t0, grp));
+            const int wb = __builtin_amdgcn_readfirstlane(wave_of(t0 + P.nblk - 1, grp));
+            // slot of wave v's piece of this tile: 0 when the tile is where v's range
+            // starts, which holds for every contributor but possibly the first
+            const int slot_wa = __builtin_amdgcn_readfirstlane(range_begin(wa, grp) >= t0 ? 0 : 1);
+            auto slot_of = [&](int v) { return v > wa ? 0 : slot_wa; };
+            const int a = max(wa, w0), b = min(wb, wlast);
+            float* mine = s_piece + (wid * 2 + (first ? 0 : 1)) * B * 64 + lane;
 #pragma unroll
-        for (int q = 0; q < S; ++q) red[q * 64] = 0.f;
-
-        auto load_item = [&](int t, int j) {
-            ItemWords w;
-            const uint8_t* tb = tb0 + static_cast<size_t>(t) * tile_bytes;
-            if (j < ng) {
-                const uint8_t* gp = tb + static_cast<size_t>(j) * tetra::kGroupBytes;
-                w.lo = *reinterpret_cast<const uint4*>(gp + 16 * lane);
-                w.hi = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * lane);
-            } else {
-                // the nblk mod 4 single columns, 384-byte runs
-                const uint8_t* sp = tb + static_cast<size_t>(ng) * tetra::kGroupBytes;
-                w.lo = make_uint4(0, 0, 0, 0);
-                w.lo.x = *reinterpret_cast<const uint32_t*>(sp + 4 * lane);
-                uint32_t h0 = *reinterpret_cast<const uint16_t*>(sp + 256 + 2 * lane), h1 = 0, h2 = 0;
-                if (rem > 1) {
-                    w.lo.y = *reinterpret_cast<const uint32_t*>(sp + kChunk + 4 * lane);
-                    h1 = *reinterpret_cast<const uint16_t*>(sp + kChunk + 256 + 2 * lane);
-                }
-                if (rem > 2) {
-                    w.lo.z = *reinterpret_cast<const uint32_t*>(sp + 2 * kChunk + 4 * lane);
-                    h2 = *reinterpret_cast<const uint16_t*>(sp + 2 * kChunk + 256 + 2 * lane);
-                }
-                w.hi = make_uint2(h0 | h1 << 16, h2);
-            }
-            return w;
-        };
-        auto advance = [&](int& t, int& j) {
-            while (j >= per_tile && t < ntr) { j -= per_tile; ++t; }
-        };
-        auto first_col = [&](int j) { return j < ng ? 4 * j : 4 * ng; };
-
-        int t = 0, j = wave;
-        advance(t, j);
-        if (t < ntr) {
-            Pipe<B> st;
-            ItemWords cw = load_item(t, j);
-            int nt = t, nj = j + kGemvWaves;
-            advance(nt, nj);
-            bool more = nt < ntr;
-            ItemWords nw = load_item(more ? nt : t, more ? nj : j);
-            {
-                uint32_t lo, hi;
-                block_word<0>(cw, lo, hi);
-                st.cur = fetch_block(lo, hi, L);
-                load_x<B>(st.x, xc, kp, first_col(j));
-                __builtin_amdgcn_s_waitcnt(0xC07F);
-            }
+            for (int bb = 0; bb < B; ++bb) mine[bb * 64] = sum[bb];
+            // LDS operations of a wave complete in order, and the last wave reads the
+            // pieces only after its own count: no fence is needed
+            uint32_t arrived = 0;
+            if (lane == 0)
+                arrived = __hip_atomic_fetch_add(s_cnt + 2 * (b - w0) + slot_of(b), 1u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
+            arrived = __builtin_amdgcn_readfirstlane(arrived);
+            if (arrived == static_cast<uint32_t>(b - a)) {
+                // last of this workgroup's pieces of the tile: add them in wave order
+                const RowTail rt = load_rows(P, t, lane);   // in flight while the sums combine
+                float tot[B];
 #pragma unroll
-            for (int bb = 0; bb < B; ++bb) st.acc[bb] = st.pdt[bb] = 0.f;
-            st.ps = 0.f;
-            st.pend_t = -1;
-            st.acc_t = t;
-            for (;;) {
-                const int ncol0 = first_col(more ? nj : j);
-                if (j < ng) {
-                    run_item<B, 4>(st, cw, nw, 4 * j, ncol0, t, L, xc, kp, red);
-                } else if (rem == 1) {
-                    run_item<B, 1>(st, cw, nw, 4 * ng, ncol0, t, L, xc, kp, red);
-                } else if (rem == 2) {
-                    run_item<B, 2>(st, cw, nw, 4 * ng, ncol0, t, L, xc, kp, red);
+                for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
+                for (int v = a; v <= b; ++v) {
+                    const float* pv = s_piece + ((v - w0) * 2 + slot_of(v)) * B * 64 + lane;
+#pragma unroll
+                    for (int bb = 0; bb < B; ++bb) tot[bb] += pv[bb * 64];
+                }
+                if (wa >= w0 && wb <= wlast) {
+                    store_rows<B>(P, t, lane, tot, rt);
                 } else {
-                    run_item<B, 3>(st, cw, nw, 4 * ng, ncol0, t, L, xc, kp, red);
-                }
-                if (!more) break;
-                t = nt;
-                j = nj;
-                cw = nw;
-                nt = t;
-                nj = j + kGemvWaves;
-                advance(nt, nj);
-                more = nt < ntr;
-                nw = load_item(more ? nt : t, more ? nj : j);
-            }
-            __builtin_amdgcn_s_waitcnt(0xC07F);
-            finish_pending<B>(st, red);
+                    // the tile reaches into other workgroups: publish this workgroup's sum.
+                    // Workgroup sums and counters are accessed only with device-scope
+                    // atomics, which are coherent across the chip's L2 caches; the wait
+                    // orders the sum before the count.
+                    const int ga = wa / kGemvWaves, gb = wb / kGemvWaves;
+                    const int gslot_ga =
+                        __builtin_amdgcn_readfirstlane(range_begin(ga * kGemvWaves, grp) >= t0 ? 0 : 1);
+                    auto gslot_of = [&](int h) { return h > ga ? 0 : gslot_ga; };
+                    float* gp = grp.partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + lane;
 #pragma unroll
-            for (int bb = 0; bb < B; ++bb) red[(st.acc_t * B + bb) * 64] = st.acc[bb];
-        }
-        __syncthreads();
-        if (wave < ntr * B) {
-            const int tt = wave / B, bb = wave - tt * B;
-            const int row = (tile0 + tt) * kTile + lane;
-            if (row < P.M) {
-                // sum in item-residue order: the wave holding items j = rho mod 16
-                // of tile tt is (rho + tt * per_tile) mod 16, so the order of the
-                // additions does not depend on how many tiles share the round
-                float tot = 0.f;
-                for (int rho = 0; rho < kGemvWaves; ++rho) {
-                    const int w = (rho + tt * per_tile) & (kGemvWaves - 1);
-                    tot += s_red[((w * S) + tt * B + bb) * 64 + lane];
+                    for (int bb = 0; bb < B; ++bb)
+                        __hip_atomic_store(gp + bb * 64, tot[bb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+                    uint32_t garr = 0;
+                    if (lane == 0)
+                        garr = __hip_atomic_fetch_add(grp.counters + gb, 1u, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
+                    garr = __builtin_amdgcn_readfirstlane(garr);
+                    if (garr == static_cast<uint32_t>(gb - ga)) {
+#pragma unroll
+                        for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
+                        // loads in batches of eight, added in workgroup order
+                        for (int h0 = ga; h0 <= gb; h0 += 8) {
+                            float pv[8][B];
+#pragma unroll
+                            for (int u = 0; u < 8; ++u) {
+                                const int h = h0 + u;
+                                if (h <= gb) {
+                                    const float* ph =
+                                        grp.partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + lane;
+#pragma unroll
+                                    for (int bb = 0; bb < B; ++bb)
+                                        pv[u][bb] = __hip_atomic_load(ph + bb * 64, __ATOMIC_RELAXED,
+                                                                      __HIP_MEMORY_SCOPE_AGENT);
+                                }
+                            }
+#pragma unroll
+                            for (int u = 0; u < 8; ++u)
+                                if (h0 + u <= gb) {
+#pragma unroll
+                                    for (int bb = 0; bb < B; ++bb) tot[bb] += pv[u][bb];
+                                }
+                        }
+                        if (lane == 0)
+                            __hip_atomic_store(grp.counters + gb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        store_rows<B>(P, t, lane, tot, rt);
+                    }
                 }
-                const uint16_t* tl =
-                    reinterpret_cast<const uint16_t*>(P.codes + P.tail_off) + static_cast<size_t>(row) * P.T;
-                const uint16_t* xt = P.x + static_cast<size_t>(bb) * P.K + 24 * nblk;
-                float ts = 0.f;
-                for (int q = 0; q < P.T; ++q) ts = fmaf(f16(tl[q]), f16(xt[q]), ts);
-                P.y[static_cast<size_t>(bb) * P.M + row] = fmaf(f16(P.sigma[row]), tot, ts);
             }
         }
-        __syncthreads();
+        i += static_cast<uint32_t>(c1 - c);
+        if (i >= end) break;
+        first = false;
+        c = 0;
+        if (++t == grp.prob[p].tiles) {
+            t = 0;
+            ++p;
+        }
+        const uint32_t left = end - i;
+        c1 = left < static_cast<uint32_t>(grp.prob[p].nblk) ? static_cast<int>(left) : grp.prob[p].nblk;
+        pc = begin_piece(grp.prob[p], t, 0, c1, lane);
     }
 }
 

@@ -24,6 +24,23 @@ constexpr int kMaxDevices = 64;
 std::mutex g_init_mu;
 bool g_init_done[kMaxDevices];
 
+// Per-device GEMV workspace (tile counters and partial sums of pieces of
+// tiles), allocated and zeroed with the tables; the counters are back at
+// zero after every launch.
+struct Workspace {
+    uint32_t* counters = nullptr;
+    float* partials = nullptr;
+    int max_waves = 0;
+};
+Workspace g_ws[kMaxDevices];
+
+int num_cus(int dev) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        return 256;
+    return n;
+}
+
 int ensure_tables(int* dev_out) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TETRA_EDEVICE;
@@ -47,6 +64,18 @@ int ensure_tables(int* dev_out) {
     if (hipMemcpyToSymbol(HIP_SYMBOL(tetra_dev::g_packed), pk, sizeof(*pk), 0, hipMemcpyHostToDevice) !=
         hipSuccess)
         return TETRA_EDEVICE;
+    Workspace& ws = g_ws[dev];
+    ws.max_waves = num_cus(dev) * tetra_dev::kGemvGroupsPerCU * tetra_dev::kGemvWaves;
+    const int max_groups = ws.max_waves / tetra_dev::kGemvWaves;
+    const size_t ws_bytes = tetra_dev::gemv_workspace_bytes(max_groups, TETRA_MAX_BATCH);
+    void* mem = nullptr;
+    if (hipMalloc(&mem, ws_bytes) != hipSuccess) return TETRA_EDEVICE;
+    if (hipMemset(mem, 0, ws_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+        (void)hipFree(mem);
+        return TETRA_EDEVICE;
+    }
+    ws.counters = static_cast<uint32_t*>(mem);
+    ws.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(mem) + sizeof(uint32_t) * max_groups);
     g_init_done[dev] = true;
     return TETRA_OK;
 }
@@ -69,13 +98,6 @@ bool shape_of(int M, int K, Shape* s) {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-int num_cus(int dev) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-        return 256;
-    return n;
-}
-
 int launch_status() { return hipGetLastError() == hipSuccess ? TETRA_OK : TETRA_EDEVICE; }
 
 int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t stream) {
@@ -83,22 +105,14 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t s
     if (batch < 1 || batch > TETRA_MAX_BATCH) return TETRA_EINVAL;
     tetra_dev::GemvGroup grp;
     std::memset(&grp, 0, sizeof(grp));
-    // longest rows first: with serpentine dealing this balances the rounds
-    int order[TETRA_MAX_GROUP];
-    Shape shapes[TETRA_MAX_GROUP];
+    unsigned long long total = 0;
     for (int i = 0; i < n; ++i) {
+        if (total >= (1ull << 31)) return TETRA_EINVAL;
         const tetra_gemv_problem& q = probs[i];
-        if (!q.codes || !q.row_scales || !q.x || !q.y || !shape_of(q.M, q.K, &shapes[i])) return TETRA_EINVAL;
+        Shape s;
+        if (!q.codes || !q.row_scales || !q.x || !q.y || !shape_of(q.M, q.K, &s)) return TETRA_EINVAL;
         if (!aligned(q.codes, 16) || !aligned(q.x, 4)) return TETRA_EALIGN;
-        order[i] = i;
-    }
-    std::stable_sort(order, order + n, [&](int a, int b) { return shapes[a].nblk > shapes[b].nblk; });
-    long long rounds = 0;
-    for (int k = 0; k < n; ++k) {
-        const int i = order[k];
-        const tetra_gemv_problem& q = probs[i];
-        const Shape& s = shapes[i];
-        tetra_dev::GemvProblem& P = grp.prob[k];
+        tetra_dev::GemvProblem& P = grp.prob[i];
         P.codes = static_cast<const uint8_t*>(q.codes);
         P.sigma = q.row_scales;
         P.x = q.x;
@@ -109,22 +123,27 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t s
         P.T = s.T;
         P.tail_off = s.tail_off;
         P.tiles = s.tiles;
-        const int items = s.nblk / 4 + (s.nblk % 4 > 0 ? 1 : 0);
-        P.round_tiles = tetra_dev::round_tiles_for(items, batch);
-        P.round_begin = static_cast<int>(rounds);
-        rounds += (s.tiles + P.round_tiles - 1) / P.round_tiles;
-        if (rounds > (1 << 30)) return TETRA_EINVAL;
+        P.ng = s.nblk / tetra::kGroupCols;
+        P.rem = s.nblk % tetra::kGroupCols;
+        P.blk_base = static_cast<uint32_t>(total);
+        total += static_cast<unsigned long long>(s.tiles) * s.nblk;
     }
-    grp.n = n;
-    grp.total_rounds = static_cast<int>(rounds);
+    if (total >= (1ull << 31)) return TETRA_EINVAL;     // block indices are 32-bit
     int dev;
     if (int st = ensure_tables(&dev)) return st;
-    const int cus = num_cus(dev);
-    const int grid = std::min(grp.total_rounds, cus * tetra_dev::gemv_wgs_per_cu(batch));
+    const Workspace& ws = g_ws[dev];
+    grp.n = n;
+    grp.total = static_cast<uint32_t>(total);
+    grp.waves = std::min(tetra_dev::gemv_waves(grp.total, num_cus(dev)), ws.max_waves);
+    grp.inv_total = 1.0 / static_cast<double>(grp.total);
+    grp.inv_waves = 1.0 / static_cast<double>(grp.waves);
+    grp.counters = ws.counters;
+    grp.partials = ws.partials;
+    const int grid = (grp.waves + tetra_dev::kGemvWaves - 1) / tetra_dev::kGemvWaves;
 #define TETRA_LAUNCH(B)                                                                           \
     case B:                                                                                       \
         hipLaunchKernelGGL(tetra_dev::gemv_kernel<B>, dim3(grid), dim3(tetra_dev::kGemvThreads), \
-                           0, stream, grp);                                                     \
+                           0, stream, grp);                                                       \
         break;
     switch (batch) {
         TETRA_LAUNCH(1) TETRA_LAUNCH(2) TETRA_LAUNCH(3) TETRA_LAUNCH(4)
