@@ -191,6 +191,38 @@ int tetra_decode(const void* words, size_t n, int8_t* y_out, float* blk_scale_ou
 int tetra_dequant(const void* codes, const uint16_t* row_scales, int M, int K,
                   float* w_out, hipStream_t stream);
 
+/*
+ * int4 projection of a served file (Sec. 4.1, Sec. 4.3): 4-bit weights in
+ * groups of 128 along K, an fp16 scale and offset per group,
+ *   w[row][k] = scale[row][k/128] * q[row][k] + offset[row][k/128],
+ *   y[b][row] = sum_k w[row][k] * x[b][k]      (f32 accumulation).
+ *   q:         device bytes [M][K/2]; element 2i in the low nibble of byte
+ *              i, 2i+1 in the high nibble; 8-byte aligned
+ *   scale_off: device fp16 [M][K/128][2] (scale, offset); 4-byte aligned
+ *   x:         device fp16 [batch][K], 16-byte aligned
+ *   y:         device fp32 [batch][M], fully overwritten
+ * K must be a positive multiple of 128; batch 1..TETRA_MAX_BATCH.
+ * Deterministic and batch-invariant.  Asynchronous; TETRA_EINVAL /
+ * TETRA_EALIGN / TETRA_EDEVICE as for tetra_gemv.
+ */
+int tetra_int4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x, float* y, int M, int K,
+                    int batch, hipStream_t stream);
+
+/*
+ * Rows of a 4-bit embedding table (Sec. 4.4): groups of 64 along the
+ * embedding dimension, fp16 scale and offset per group, nibbles as in
+ * tetra_int4_gemv;  out[i][k] = fl32(fl32(scale * q) + offset) for the row
+ * tokens[i].
+ *   q:         device bytes [rows][dim/2]
+ *   scale_off: device fp16 [rows][dim/64][2]
+ *   tokens:    device int32 [n]; a token outside [0, rows) gives a row of
+ *              zeros (the table is never read out of bounds)
+ *   out:       device fp32 [n][dim]
+ * dim must be a positive multiple of 64.  Asynchronous.
+ */
+int tetra_emb4_gather(const void* q, const uint16_t* scale_off, int rows, int dim, const int* tokens, int n,
+                      float* out, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -35,6 +35,8 @@ _SIGNATURES = {
     "tetra_gemv_grouped": (_int, [_vp, _int, _int, _vp]),
     "tetra_decode": (_int, [_vp, _sz, _vp, _vp, _vp]),
     "tetra_dequant": (_int, [_vp, _vp, _int, _int, _vp, _vp]),
+    "tetra_int4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
+    "tetra_emb4_gather": (_int, [_vp, _vp, _int, _int, _vp, _int, _vp, _vp]),
 }
 EXPORTED = tuple(_SIGNATURES)
 
@@ -166,3 +168,17 @@ def decode(words_bytes, n: int, y_out, scale_out=None, stream=None):
 def dequant(codes, row_scales, M: int, K: int, w_out, stream=None):
     _check(_call("tetra_dequant", _ptr(codes), _ptr(row_scales), M, K, _ptr(w_out),
                         _stream(stream)), "tetra_dequant")
+
+
+def int4_gemv(q, scale_off, x, y, M: int, K: int, batch: int = 1, stream=None):
+    """y[batch, M] for an int4 projection: q uint8 [M, K/2], scale_off fp16
+    [M, K/128, 2], x fp16 [batch, K] (all device tensors)."""
+    _check(_call("tetra_int4_gemv", _ptr(q), _ptr(scale_off), _ptr(x), _ptr(y), M, K, batch,
+                 _stream(stream)), "tetra_int4_gemv")
+
+
+def emb4_gather(q, scale_off, rows: int, dim: int, tokens, out, stream=None):
+    """out[n, dim] fp32 = rows tokens[n] (int32 device tensor) of a 4-bit
+    embedding table q uint8 [rows, dim/2], scale_off fp16 [rows, dim/64, 2]."""
+    _check(_call("tetra_emb4_gather", _ptr(q), _ptr(scale_off), rows, dim, _ptr(tokens),
+                 int(tokens.numel()), _ptr(out), _stream(stream)), "tetra_emb4_gather")

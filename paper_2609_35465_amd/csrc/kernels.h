@@ -692,4 +692,138 @@ void gemv_kernel(const GemvGroup grp) {
     }
 }
 
+// ----------------------------------------------------- int4 projections
+//
+// The int4 records of a served file (Sec. 4.1, Sec. 4.3): 4-bit weights in
+// groups of 128 along K with an fp16 scale and offset per group,
+// w = scale * q + offset, q the unsigned nibble (element 2i in the low
+// nibble of byte i).  Per group the product is
+//   sum_k w_k x_k = scale * sum_k q_k x_k + offset * sum_k x_k,
+// so the nibbles go to fp16 unscaled and the group's scale and offset are
+// applied once.
+//
+// Layout: q [M][K/2] bytes, scale/offset [M][K/128][2] fp16, both row-major.
+// A wave takes 4 rows at a time and walks K in steps of 1024 weights, 16 per
+// lane (8 bytes of q per row, coalesced into 512-byte runs); the lane's 16
+// activations are loaded once per step for the 4 rows.  Nibble k of a dword
+// and nibble k+4 become one fp16 pair with a single and-or against the bits
+// of 1024.0 (giving 1024 + q exactly); the activation pairs are permuted to
+// match, and 1024 times the lane's activation sum is taken back out.  Lanes
+// are added with a fixed butterfly, so results are deterministic and
+// batch-invariant.
+
+constexpr int kInt4Group = 128;
+constexpr int kInt4RowsPerWave = 4;
+constexpr int kInt4Waves = 4;
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+template <int B>
+__global__ __launch_bounds__(kInt4Waves * 64) void int4_gemv_kernel(const uint8_t* __restrict__ q,
+                                                                   const uint16_t* __restrict__ so,
+                                                                   const uint16_t* __restrict__ x,
+                                                                   float* __restrict__ y, int M, int K) {
+    const int lane = threadIdx.x & 63;
+    const int wave = blockIdx.x * kInt4Waves + (threadIdx.x >> 6);
+    const int r0 = wave * kInt4RowsPerWave;
+    if (r0 >= M) return;
+    const int groups = K / kInt4Group;
+    float acc[kInt4RowsPerWave][B];
+#pragma unroll
+    for (int r = 0; r < kInt4RowsPerWave; ++r)
+#pragma unroll
+        for (int bb = 0; bb < B; ++bb) acc[r][bb] = 0.f;
+    for (int k0 = 16 * lane; k0 < K; k0 += 1024) {
+        // activations of this lane's 16 weights, paired (k, k+4) within each 8
+        uint32_t xp[B][8];
+        float sx[B];
+#pragma unroll
+        for (int bb = 0; bb < B; ++bb) {
+            const uint4* xs = reinterpret_cast<const uint4*>(x + static_cast<size_t>(bb) * K + k0);
+            const uint4 a = xs[0], b = xs[1];
+            const uint32_t n[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};   // pairs (2i, 2i+1)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                // elements 8h..8h+7: natural pairs n[4h..4h+3]; wanted (e, e+4) for e = 0..3
+                xp[bb][4 * h + 0] = __builtin_amdgcn_perm(n[4 * h + 2], n[4 * h + 0], 0x05040100u);
+                xp[bb][4 * h + 1] = __builtin_amdgcn_perm(n[4 * h + 2], n[4 * h + 0], 0x07060302u);
+                xp[bb][4 * h + 2] = __builtin_amdgcn_perm(n[4 * h + 3], n[4 * h + 1], 0x05040100u);
+                xp[bb][4 * h + 3] = __builtin_amdgcn_perm(n[4 * h + 3], n[4 * h + 1], 0x07060302u);
+            }
+            float s = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) s = dot2(n[i], 0x3C003C00u, s);
+            sx[bb] = s;
+        }
+        const int g = k0 / kInt4Group;
+#pragma unroll
+        for (int r = 0; r < kInt4RowsPerWave; ++r) {
+            const int row = min(r0 + r, M - 1);
+            const uint2 w = *reinterpret_cast<const uint2*>(q + static_cast<size_t>(row) * (K >> 1) + (k0 >> 1));
+            const uint32_t sov = *reinterpret_cast<const uint32_t*>(so + (static_cast<size_t>(row) * groups + g) * 2);
+            const float sc = f16(static_cast<uint16_t>(sov)), of = f16(static_cast<uint16_t>(sov >> 16));
+            uint32_t np[8];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const uint32_t d = h ? w.y : w.x;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    np[4 * h + e] = ((d >> (4 * e)) & 0x000F000Fu) | 0x64006400u;   // (1024 + q_e, 1024 + q_{e+4})
+            }
+#pragma unroll
+            for (int bb = 0; bb < B; ++bb) {
+                float dt = 0.f;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) dt = dot2(np[i], xp[bb][i], dt);
+                // sum q x = dt - 1024 sx; times scale, plus offset * sx
+                acc[r][bb] = fmaf(sc, fmaf(-1024.f, sx[bb], dt), fmaf(of, sx[bb], acc[r][bb]));
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kInt4RowsPerWave; ++r)
+#pragma unroll
+        for (int bb = 0; bb < B; ++bb) {
+            const float v = wave_sum(acc[r][bb]);
+            if (lane == 0 && r0 + r < M) y[static_cast<size_t>(bb) * M + r0 + r] = v;
+        }
+}
+
+// ------------------------------------------------ 4-bit embedding rows
+//
+// One row of a 4-bit embedding table (Sec. 4.4): groups of 64 along the
+// embedding dimension, fp16 scale and offset per group, same nibble order;
+// out[k] = fl32(fl32(scale * q_k) + offset).  One thread per byte.
+
+constexpr int kEmbGroup = 64;
+
+__global__ __launch_bounds__(256) void emb4_gather_kernel(const uint8_t* __restrict__ q,
+                                                          const uint16_t* __restrict__ so, int rows, int dim,
+                                                          const int* __restrict__ tokens, int n,
+                                                          float* __restrict__ out) {
+    const int half = dim >> 1;
+    for (long long i = blockIdx.x * static_cast<long long>(blockDim.x) + threadIdx.x;
+         i < static_cast<long long>(n) * half; i += static_cast<long long>(gridDim.x) * blockDim.x) {
+        const int tok_i = static_cast<int>(i / half), b = static_cast<int>(i - static_cast<long long>(tok_i) * half);
+        const long long row = tokens[tok_i];
+        const int k = 2 * b;
+        float* o = out + static_cast<long long>(tok_i) * dim + k;
+        if (row < 0 || row >= rows) {     // a token outside the table gives zeros
+            o[0] = 0.f;
+            o[1] = 0.f;
+            continue;
+        }
+        const uint32_t v = q[row * half + b];
+        const uint32_t sov =
+            *reinterpret_cast<const uint32_t*>(so + (row * (dim / kEmbGroup) + k / kEmbGroup) * 2);
+        const float sc = f16(static_cast<uint16_t>(sov)), of = f16(static_cast<uint16_t>(sov >> 16));
+        o[0] = __fadd_rn(__fmul_rn(sc, static_cast<float>(v & 15u)), of);
+        o[1] = __fadd_rn(__fmul_rn(sc, static_cast<float>(v >> 4)), of);
+    }
+}
+
 }  // namespace tetra_dev

@@ -290,4 +290,43 @@ int tetra_dequant(const void* codes, const uint16_t* row_scales, int M, int K, f
     return launch_status();
 }
 
+int tetra_int4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x, float* y, int M, int K,
+                    int batch, hipStream_t stream) {
+    if (!q || !scale_off || !x || !y || M < 1 || K < tetra_dev::kInt4Group || K % tetra_dev::kInt4Group)
+        return TETRA_EINVAL;
+    if (batch < 1 || batch > TETRA_MAX_BATCH) return TETRA_EINVAL;
+    if (!aligned(q, 8) || !aligned(scale_off, 4) || !aligned(x, 16)) return TETRA_EALIGN;
+    int dev;
+    if (int st = ensure_tables(&dev)) return st;
+    const long long waves = (static_cast<long long>(M) + tetra_dev::kInt4RowsPerWave - 1) / tetra_dev::kInt4RowsPerWave;
+    const unsigned grid = static_cast<unsigned>((waves + tetra_dev::kInt4Waves - 1) / tetra_dev::kInt4Waves);
+    const uint8_t* qb = static_cast<const uint8_t*>(q);
+#define TETRA_I4(B)                                                                                        \
+    case B:                                                                                                \
+        hipLaunchKernelGGL(tetra_dev::int4_gemv_kernel<B>, dim3(grid), dim3(tetra_dev::kInt4Waves * 64), 0, \
+                           stream, qb, scale_off, x, y, M, K);                                             \
+        break;
+    switch (batch) {
+        TETRA_I4(1) TETRA_I4(2) TETRA_I4(3) TETRA_I4(4) TETRA_I4(5) TETRA_I4(6) TETRA_I4(7) TETRA_I4(8)
+        default: return TETRA_EINVAL;
+    }
+#undef TETRA_I4
+    return launch_status();
+}
+
+int tetra_emb4_gather(const void* q, const uint16_t* scale_off, int rows, int dim, const int* tokens, int n,
+                      float* out, hipStream_t stream) {
+    if (!q || !scale_off || !tokens || !out || rows < 1 || n < 1 || dim < tetra_dev::kEmbGroup ||
+        dim % tetra_dev::kEmbGroup)
+        return TETRA_EINVAL;
+    if (!aligned(scale_off, 4) || !aligned(tokens, 4) || !aligned(out, 4)) return TETRA_EALIGN;
+    int dev;
+    if (int st = ensure_tables(&dev)) return st;
+    const long long bytes = static_cast<long long>(n) * (dim / 2);
+    const unsigned grid = static_cast<unsigned>(std::min<long long>((bytes + 255) / 256, 4096));
+    hipLaunchKernelGGL(tetra_dev::emb4_gather_kernel, dim3(grid), dim3(256), 0, stream,
+                       static_cast<const uint8_t*>(q), scale_off, rows, dim, tokens, n, out);
+    return launch_status();
+}
+
 }  // extern "C"

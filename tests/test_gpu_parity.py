@@ -243,3 +243,125 @@ def test_gemv_config_sampled_rows(config, batch):
         x = workloads.activations(workloads.seed_for(config, idx), batch, K)
         _check_gemv(pk, x, rows=_sample_rows(M, rng), label=f"c{config}:{name}")
         del pk
+
+
+# ------------------------------------------------------------- determinism
+
+def test_gemv_repeat_is_bitwise_identical():
+    """Pieces of row tiles are added in a fixed order: repeated launches give
+    the same bits (tiles here are split over many waves and workgroups)."""
+    M, K = 640, 24 * 213 + 8
+    words, sigma, tail = workloads.tetra_matrix(31, M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(31, 2, K)
+    first = pk.gemv(x)
+    for _ in range(5):
+        assert np.array_equal(pk.gemv(x), first)
+
+
+# ------------------------------------------------------------------- int4
+
+from oracle import int4 as oint4  # noqa: E402
+
+
+def _int4_check(M, K, batch, seed, rows=None):
+    q, so = workloads.int4_matrix(seed, M, K)
+    x = workloads.activations(seed, batch, K)
+    y = torch.empty((batch, M), dtype=torch.float32, device="cuda")
+    tt.int4_gemv(_dev(q), _f16_dev(so), _f16_dev(x), y, M, K, batch)
+    torch.cuda.synchronize()
+    yg = y.cpu().numpy().astype(np.float64)
+    yr, norm = oint4.int4_gemv_f64(q, so, x, rows=rows)
+    if rows is not None:
+        yg = yg[:, rows]
+    worst = float((np.abs(yg - yr) / np.maximum(norm, 1e-300)).max())
+    print(f"[int4] M={M} K={K} batch={batch} worst={worst:.3e}", flush=True)
+    assert worst <= TOL
+    assert worst <= TOL_PAPER
+    return y.cpu().numpy(), x, q, so
+
+
+@pytest.mark.parametrize("M,K", [(1, 128), (5, 384), (130, 1024), (64, 5120), (33, 1152), (7, 17408)])
+def test_int4_gemv_small(M, K):
+    _int4_check(M, K, 1, 600 + M)
+
+
+@pytest.mark.parametrize("batch", [1, 2, 3, 4, 8])
+def test_int4_gemv_batches_are_invariant(batch):
+    M, K = 72, 2560
+    yb, x, q, so = _int4_check(M, K, batch, 700 + batch)
+    for b in range(batch):
+        y1 = torch.empty((1, M), dtype=torch.float32, device="cuda")
+        tt.int4_gemv(_dev(q), _f16_dev(so), _f16_dev(x[b:b + 1]), y1, M, K, 1)
+        torch.cuda.synchronize()
+        assert np.array_equal(y1.cpu().numpy()[0], yb[b])
+
+
+def test_int4_gemv_degenerate():
+    M, K = 40, 512
+    q = np.zeros((M, K // 2), np.uint8)
+    so = np.zeros((M, K // 128, 2), np.float16)
+    so[..., 0] = 0.25
+    so[..., 1] = np.linspace(-1, 1, M * (K // 128)).reshape(M, K // 128)
+    # q = 0: only the offsets remain; x = e_k picks offset[row][k / 128]
+    for k in (0, 127, 128, 511):
+        e = np.zeros((1, K), np.float16)
+        e[0, k] = 1.0
+        y = torch.empty((1, M), dtype=torch.float32, device="cuda")
+        tt.int4_gemv(_dev(q), _f16_dev(so), _f16_dev(e), y, M, K, 1)
+        torch.cuda.synchronize()
+        assert np.array_equal(y.cpu().numpy()[0], so[:, k // 128, 1].astype(np.float32))
+
+
+@pytest.mark.parametrize("name", ["q", "k", "o", "gate", "down"])
+def test_int4_gemv_14b_shapes_sampled(name):
+    shapes = {n: (M, K) for n, M, K in workloads.layer_shapes("14B")}
+    M, K = shapes[name]
+    rng = np.random.default_rng(len(name))
+    _int4_check(M, K, 1, 800 + M + K, rows=_sample_rows(M, rng))
+
+
+# ------------------------------------------------------------------- emb4
+
+def test_emb4_gather_bit_exact():
+    rows, dim = 3000, 5120
+    q, so, token = workloads.emb4_table(5, rows, dim)
+    toks = np.array([0, rows - 1, token, 17, token], np.int32)
+    out = torch.empty((len(toks), dim), dtype=torch.float32, device="cuda")
+    tt.emb4_gather(_dev(q), _f16_dev(so), rows, dim, _dev(toks), out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    for i, t in enumerate(toks):
+        want = oint4.emb4_row(q, so, int(t))
+        assert np.array_equal(got[i].view(np.uint32), want.view(np.uint32)), t
+
+
+def test_emb4_gather_out_of_range_tokens_give_zeros():
+    rows, dim = 10, 128
+    q, so, _ = workloads.emb4_table(6, rows, dim)
+    toks = np.array([-1, rows, 3], np.int32)
+    out = torch.full((3, dim), 7.0, dtype=torch.float32, device="cuda")
+    tt.emb4_gather(_dev(q), _f16_dev(so), rows, dim, _dev(toks), out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    assert not got[0].any() and not got[1].any()
+    assert np.array_equal(got[2], oint4.emb4_row(q, so, 3))
+
+
+def test_emb4_gather_full_size_table():
+    """The 151,936 x 5,120 table of the 14B shapes, made on the device; the
+    checked rows are copied back for the oracle."""
+    rows, dim = 151936, 5120
+    g = torch.Generator(device="cuda").manual_seed(11)
+    qd = torch.empty((rows, dim // 2), dtype=torch.uint8, device="cuda").random_(0, 256, generator=g)
+    sod = (torch.rand((rows, dim // 64, 2), generator=g, device="cuda") * 0.02).half()
+    toks = np.array([0, 1, 77777, rows - 1], np.int32)
+    out = torch.empty((len(toks), dim), dtype=torch.float32, device="cuda")
+    tt.emb4_gather(qd, sod, rows, dim, _dev(toks), out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    for i, t in enumerate(toks):
+        qr = qd[int(t)].cpu().numpy()[None]
+        sr = sod[int(t)].cpu().numpy()[None]
+        want = oint4.emb4_row(qr, sr, 0)
+        assert np.array_equal(got[i].view(np.uint32), want.view(np.uint32)), t
