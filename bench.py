@@ -52,6 +52,10 @@ def parse():
                     help="matrix: one launch per matrix; deps: per layer [q,k,v] [o] "
                          "[gate,up] [down] (the launches a decode step can fuse); "
                          "layer: one grouped launch per layer")
+    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4"],
+                    help="tetra: every projection a Tetra matrix (the GEMV metric); c4: the "
+                         "full decode step -- 10%% of the projections (seeded) stored as int4 "
+                         "w4g128 and one 4-bit embedding row gathered per step")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the benchmark: copy a buffer of this many MiB five "
                          "times with torch (a plain copy kernel of known size, the "
@@ -84,20 +88,57 @@ class Matrix:
         self.weights = M * K
 
 
-def build_workload(torch, tt, model, layers, batch):
+class Int4Matrix:
+    """One int4 (w4g128, fp16 scale/offset per group) projection on the GPU."""
+
+    def __init__(self, torch, name, M, K, gen):
+        self.name, self.M, self.K = name, M, K
+        self.q = torch.empty((M, K // 2), dtype=torch.uint8, device="cuda").random_(0, 256, generator=gen)
+        scale = (torch.rand((M, K // 128), generator=gen, device="cuda") * 1.5 + 0.5) * (1e-2 / 8)
+        self.so = torch.stack([scale, -7.5 * scale], dim=-1).half().contiguous()
+        self.read_bytes = M * K // 2 + M * (K // 128) * 4
+        self.weights = M * K
+
+
+class Emb4Table:
+    """The 4-bit embedding table (groups of 64) and the token gathered per step."""
+
+    def __init__(self, torch, rows, dim, gen, token):
+        self.rows, self.dim = rows, dim
+        self.q = torch.empty((rows, dim // 2), dtype=torch.uint8, device="cuda").random_(0, 256, generator=gen)
+        scale = (torch.rand((rows, dim // 64), generator=gen, device="cuda") * 1.5 + 0.5) * (1e-2 / 8)
+        self.so = torch.stack([scale, -7.5 * scale], dim=-1).half().contiguous()
+        self.tokens = torch.tensor([token], dtype=torch.int32, device="cuda")
+        self.out = torch.empty((1, dim), dtype=torch.float32, device="cuda")
+        self.read_bytes = dim // 2 + (dim // 64) * 4
+
+
+def build_workload(torch, tt, model, layers, batch, workload="tetra"):
     from paper_2609_35465_amd import workloads
     shapes = workloads.layer_shapes(model)
     L = layers or workloads.QWEN3[model]["layers"]
     gen = torch.Generator(device="cuda").manual_seed(workloads.SEED_BASE + 3)
+    n_total = L * len(shapes)
+    int4_set = set()
+    if workload == "c4":
+        int4_set = set(workloads.int4_pick(workloads.SEED_BASE + 4, n_total).tolist())
     mats, xs, ys = [], {}, []
     for layer in range(L):
         for i, (name, M, K) in enumerate(shapes):
-            mats.append(Matrix(torch, tt, name, M, K, gen, workloads.seed_for(3, 16 * layer + i)))
+            li = layer * len(shapes) + i
+            if li in int4_set:
+                mats.append(Int4Matrix(torch, name, M, K, gen))
+            else:
+                mats.append(Matrix(torch, tt, name, M, K, gen, workloads.seed_for(3, 16 * layer + i)))
             if (layer, K) not in xs:
                 xs[(layer, K)] = torch.randn(batch, K, generator=gen, device="cuda").half()
             ys.append(torch.empty(batch, M, dtype=torch.float32, device="cuda"))
     plan = [(m, xs[(li // len(shapes), m.K)], ys[li]) for li, m in enumerate(mats)]
-    return plan, L
+    emb = None
+    if workload == "c4":
+        q = workloads.QWEN3[model]
+        emb = Emb4Table(torch, 151936, q["hidden"], gen, token=int(workloads.SEED_BASE % 151936))
+    return plan, L, emb
 
 
 GROUPS = {
@@ -107,22 +148,39 @@ GROUPS = {
 }
 
 
-def build_launches(tt, plan, mode, nproj=7):
-    """One ctypes problem array per launch, in step order."""
+def build_launches(tt, plan, mode, nproj=7, emb=None):
+    """Launches of one step, in order: ("tetra", problem array, matrices),
+    ("int4", matrix, x, y) or ("emb4", table)."""
     launches = []
+    if emb is not None:
+        launches.append(("emb4", emb))
     for l0 in range(0, len(plan), nproj):
         layer = plan[l0:l0 + nproj]
         by_name = {m.name: (m, x, y) for m, x, y in layer}
         for names in GROUPS[mode]:
-            items = [(by_name[n][0].blob, by_name[n][0].sigma, by_name[n][1], by_name[n][2],
-                      by_name[n][0].M, by_name[n][0].K) for n in names]
-            launches.append((tt.make_problems(items), [by_name[n][0] for n in names]))
+            tet = [n for n in names if isinstance(by_name[n][0], Matrix)]
+            if tet:
+                items = [(by_name[n][0].blob, by_name[n][0].sigma, by_name[n][1], by_name[n][2],
+                          by_name[n][0].M, by_name[n][0].K) for n in tet]
+                launches.append(("tetra", tt.make_problems(items), [by_name[n][0] for n in tet]))
+            for n in names:
+                if not isinstance(by_name[n][0], Matrix):
+                    launches.append(("int4",) + by_name[n])
     return launches
 
 
-def run_step(tt, launches, batch, stream):
-    for probs, _ in launches:
-        tt.gemv_grouped(probs, batch, stream)
+def run_step(tt, launches, batch, stream, only_tetra=False):
+    for ln in launches:
+        if ln[0] == "tetra":
+            tt.gemv_grouped(ln[1], batch, stream)
+        elif only_tetra:
+            continue
+        elif ln[0] == "int4":
+            m, x, y = ln[1:]
+            tt.int4_gemv(m.q, m.so, x, y, m.M, m.K, batch, stream)
+        else:
+            e = ln[1]
+            tt.emb4_gather(e.q, e.so, e.rows, e.dim, e.tokens, e.out, stream)
 
 
 def parity_spot_check(torch, tt, plan, batch):
@@ -131,7 +189,7 @@ def parity_spot_check(torch, tt, plan, batch):
     worst = 0.0
     seen = set()
     for m, x, y in plan:
-        if m.name in seen:
+        if m.name in seen or not isinstance(m, Matrix):
             continue
         seen.add(m.name)
         rows = np.unique(np.r_[0:8, m.M - 8:m.M, np.linspace(0, m.M - 1, 24).astype(int)])
@@ -140,6 +198,21 @@ def parity_spot_check(torch, tt, plan, batch):
         sig = m.sigma.cpu().numpy()
         xh = x.cpu().numpy()
         ref, norm = ogemv.gemv_f64(words, sig, tail, xh, rows=rows)
+        got = y.cpu().numpy()[:, rows].astype(np.float64)
+        worst = max(worst, float((np.abs(got - ref) / norm).max()))
+    return worst
+
+
+def parity_spot_check_int4(torch, plan):
+    """Sampled rows of each int4 shape against the oracle (worst relative error)."""
+    from oracle import int4 as oint4
+    worst, seen = 0.0, set()
+    for m, x, y in plan:
+        if isinstance(m, Matrix) or m.name in seen:
+            continue
+        seen.add(m.name)
+        rows = np.unique(np.r_[0:8, m.M - 8:m.M, np.linspace(0, m.M - 1, 24).astype(int)])
+        ref, norm = oint4.int4_gemv_f64(m.q.cpu().numpy(), m.so.cpu().numpy(), x.cpu().numpy(), rows=rows)
         got = y.cpu().numpy()[:, rows].astype(np.float64)
         worst = max(worst, float((np.abs(got - ref) / norm).max()))
     return worst
@@ -155,6 +228,8 @@ def cpu_baseline(torch, tt, plan, seconds):
     for m, x, _ in plan:
         if t_used >= seconds:
             break
+        if not isinstance(m, Matrix):
+            continue
         blob = m.blob.cpu().numpy()
         words, tail = tt.unpack_rows(blob, m.M, m.K)
         sig = m.sigma.cpu().numpy()
@@ -206,7 +281,8 @@ def recorded_traffic(args, layers):
             k, v = line[2:].strip().split(": ", 1)
             rec[k] = v.strip().strip("`")
     want = {"source_sha256": kernel_source_hash(), "mode": args.mode,
-            "batch": str(args.batch), "model": args.model, "layers": str(layers)}
+            "batch": str(args.batch), "model": args.model, "layers": str(layers),
+            "workload": args.workload}
     if any(rec.get(k) != v for k, v in want.items()):
         return None
     try:
@@ -238,58 +314,72 @@ def main():
         print(json.dumps({"copy_probe_bytes": n, "copies": 5}), flush=True)
         return 0
     stream = torch.cuda.current_stream()
-    plan, L = build_workload(torch, tt, args.model, args.layers, args.batch)
+    plan, L, emb = build_workload(torch, tt, args.model, args.layers, args.batch, args.workload)
     torch.cuda.synchronize()
 
-    bytes_read = sum(m.read_bytes for m, _, _ in plan)
+    tetra = [(m, x, y) for m, x, y in plan if isinstance(m, Matrix)]
+    bytes_read = sum(m.read_bytes for m, _, _ in plan) + (emb.read_bytes if emb else 0)
     bytes_xy = sum(2 * m.K * args.batch + 4 * m.M * args.batch for m, _, _ in plan)
     weights = sum(m.weights for m, _, _ in plan)
     algo_bytes = bytes_read + bytes_xy
+    tetra_bytes = sum(m.read_bytes + 2 * m.K * args.batch + 4 * m.M * args.batch for m, _, _ in tetra)
 
-    launches = build_launches(tt, plan, args.mode)
-    # warm-up (also uploads the decoder tables)
+    launches = build_launches(tt, plan, args.mode, emb=emb)
+    n_tetra = sum(1 for ln in launches if ln[0] == "tetra")
+    # warm-up (also uploads the decoder tables and sets up the workspace)
     for _ in range(max(1, args.warmup)):
         run_step(tt, launches, args.batch, stream.cuda_stream)
     torch.cuda.synchronize()
     parity = parity_spot_check(torch, tt, plan, args.batch)
+    parity_int4 = parity_spot_check_int4(torch, plan) if args.workload == "c4" else None
 
-    graph = None
-    if not args.no_graph:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            run_step(tt, launches, args.batch, torch.cuda.current_stream().cuda_stream)
+    def capture(only_tetra):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run_step(tt, launches, args.batch, torch.cuda.current_stream().cuda_stream, only_tetra)
         # replays must reproduce the eager result
-        ref = [y.clone() for _, _, y in plan[:7]]
+        check = [(m, x, y) for m, x, y in plan[:7] if isinstance(m, Matrix) or not only_tetra]
+        ref = [y.clone() for _, _, y in check]
         for _ in range(3):
-            for _, _, y in plan[:7]:
+            for _, _, y in check:
                 y.zero_()
-            graph.replay()
+            g.replay()
             torch.cuda.synchronize()
-            for r, (_, _, y) in zip(ref, plan[:7]):
+            for r, (_, _, y) in zip(ref, check):
                 assert torch.equal(r, y), "graph replay differs from the eager run"
+        return g
 
-    def step():
-        if graph is not None:
-            graph.replay()
-        else:
-            run_step(tt, launches, args.batch, stream.cuda_stream)
+    graph = None if args.no_graph else capture(False)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / args.steps
+    def timed(step, steps):
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
 
-    # average gemv_kernel launch over the timed region (HIP events on the
-    # launch stream; the step is nothing but back-to-back gemv launches)
-    avg_launch_ms = ms_step / len(launches)
-    achieved = (algo_bytes / len(launches)) / (avg_launch_ms * 1e-3) / 1e9
+    if graph is not None:
+        ms_step = timed(graph.replay, args.steps)
+    else:
+        ms_step = timed(lambda: run_step(tt, launches, args.batch, stream.cuda_stream), args.steps)
+
+    # average gemv_kernel launch over a timed region of back-to-back gemv
+    # launches (HIP events on the launch stream): the step itself for the
+    # all-Tetra workload, a Tetra-only replay of the same step otherwise
+    if args.workload == "tetra":
+        tetra_ms = ms_step
+    elif graph is not None:
+        tetra_ms = timed(capture(True).replay, args.steps)
+    else:
+        tetra_ms = timed(lambda: run_step(tt, launches, args.batch, stream.cuda_stream, True), args.steps)
+    avg_launch_ms = tetra_ms / n_tetra
+    achieved = (tetra_bytes / n_tetra) / (avg_launch_ms * 1e-3) / 1e9
     traffic = recorded_traffic(args, L)
 
     value = algo_bytes / (ms_step * 1e-3) / 1e9
@@ -308,9 +398,13 @@ def main():
         "dtype": "f16-in/f32-acc",
         "data": "synthetic",
         "config": {
-            "workload": f"Qwen3-{args.model}-shaped linear set x {L} layers "
-                        f"({len(plan)} Tetra matrices), batch {args.batch}, one token-equivalent pass",
-            "batch": args.batch, "layers": L, "matrices": len(plan),
+            "workload": (f"Qwen3-{args.model}-shaped linear set x {L} layers "
+                         f"({len(tetra)} Tetra matrices), batch {args.batch}, one token-equivalent pass"
+                         if args.workload == "tetra" else
+                         f"Qwen3-{args.model}-shaped decode step: {L} layers, {len(tetra)} Tetra + "
+                         f"{len(plan) - len(tetra)} int4 w4g128 matrices, one 4-bit embedding row of "
+                         f"151936 x {emb.dim}, batch {args.batch}"),
+            "batch": args.batch, "layers": L, "matrices": len(plan), "tetra_matrices": len(tetra),
             "hip_graph": graph is not None, "launches_per_step": len(launches),
             "launch_grouping": args.mode,
         },
@@ -319,11 +413,12 @@ def main():
         "weights_per_s": round(weights / (ms_step * 1e-3), 1),
         "token_equiv_latency_ms": round(ms_step, 4),
         "parity_worst_rel_err": parity,
+        "parity_int4_worst_rel_err": parity_int4,
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
             "kernel": "gemv_kernel", "avg_launch_us": round(avg_launch_ms * 1e3, 3),
-            "bytes_per_launch": round(algo_bytes / len(launches)),
+            "bytes_per_launch": round(tetra_bytes / n_tetra),
         },
     }
     if not args.no_cpu_baseline:
