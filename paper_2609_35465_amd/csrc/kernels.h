@@ -11,9 +11,9 @@ namespace tetra_dev {
 
 constexpr int kTile = 64;                 // rows per code tile = lanes per wave
 constexpr int kChunk = kTile * 6;         // bytes per (tile, block column) chunk
-constexpr int kGemvWaves = 8;                  // waves per GEMV workgroup
+constexpr int kGemvWaves = 12;                 // waves per GEMV workgroup
 constexpr int kGemvThreads = kGemvWaves * 64;
-constexpr int kGemvGroupsPerCU = 3;            // at batch 1: 3 x 54.5 KB of LDS, 6 waves per SIMD
+constexpr int kGemvGroupsPerCU = 2;            // at batch 1: 2 x 56.5 KB of LDS, 6 waves per SIMD
 constexpr int kMaxGroup = 16;
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
@@ -272,7 +272,7 @@ struct GemvGroup {
     int n, waves;
 };
 
-// wave count of a launch: three 512-thread workgroups per CU, fewer when
+// wave count of a launch: two 768-thread workgroups per CU, fewer when
 // there are fewer blocks than waves (every wave's range must be non-empty);
 // independent of the batch size
 inline int gemv_waves(uint32_t total, int cus) {
