@@ -23,6 +23,15 @@ __device__ __forceinline__ float f16(uint16_t v) {
     return static_cast<float>(__builtin_bit_cast(_Float16, v));
 }
 
+// the lane index, computed afresh at each use: the cold paths of the GEMV
+// (tile tails, single columns, piece reduction) take their lane addresses
+// from it, so that none of them is hoisted and kept live across the hot loop
+__device__ __forceinline__ int lane_now() {
+    int l;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+    return l;
+}
+
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, a), __builtin_bit_cast(half2_t, b), c,
                                   false);
@@ -272,12 +281,16 @@ struct GemvGroup {
     int n, waves;
 };
 
-// wave count of a launch: two 768-thread workgroups per CU, fewer when
-// there are fewer blocks than waves (every wave's range must be non-empty);
-// independent of the batch size
+// wave count of a launch: two 768-thread workgroups per CU, fewer when the
+// launch is small, so that each wave takes at least kGemvMinBlocks blocks (a
+// wave's fixed cost, table staging and its share of the piece reduction, is
+// worth several blocks of streaming; every range is non-empty); independent
+// of the batch size
+constexpr uint32_t kGemvMinBlocks = 8;
 inline int gemv_waves(uint32_t total, int cus) {
     const uint32_t cap = static_cast<uint32_t>(cus) * kGemvGroupsPerCU * kGemvWaves;
-    return static_cast<int>(total < cap ? total : cap);
+    const uint32_t want = total / kGemvMinBlocks > 0 ? total / kGemvMinBlocks : 1u;
+    return static_cast<int>(want < cap ? want : cap);
 }
 
 // workspace bytes for G workgroups at batch B: a counter and two partial
@@ -419,6 +432,7 @@ __device__ __forceinline__ ItemWords load_item(const uint8_t* tb, int j, int ng,
     } else {
         // the nblk mod 4 single columns, 384-byte runs
         const uint8_t* sp = tb + static_cast<size_t>(ng) * tetra::kGroupBytes;
+        lane = lane_now();
         w.lo = make_uint4(0, 0, 0, 0);
         w.lo.x = *reinterpret_cast<const uint32_t*>(sp + 4 * lane);
         uint32_t h0 = *reinterpret_cast<const uint16_t*>(sp + 256 + 2 * lane), h1 = 0, h2 = 0;
@@ -523,9 +537,9 @@ struct RowTail {
     float sg;
 };
 
-__device__ __forceinline__ RowTail load_rows(const GemvProblem& P, int t, int lane) {
+__device__ __forceinline__ RowTail load_rows(const GemvProblem& P, int t) {
     RowTail r;
-    const int row = min(t * kTile + lane, P.M - 1);
+    const int row = min(t * kTile + lane_now(), P.M - 1);
     const uint32_t* tl =
         reinterpret_cast<const uint32_t*>(P.codes + P.tail_off) + static_cast<size_t>(row) * (P.T >> 1);
     r.sg = f16(P.sigma[row]);
@@ -535,9 +549,8 @@ __device__ __forceinline__ RowTail load_rows(const GemvProblem& P, int t, int la
 }
 
 template <int B>
-__device__ __forceinline__ void store_rows(const GemvProblem& P, int t, int lane, const float (&tot)[B],
-                                           const RowTail& r) {
-    const int row = t * kTile + lane;
+__device__ __forceinline__ void store_rows(const GemvProblem& P, int t, const float (&tot)[B], const RowTail& r) {
+    const int row = t * kTile + lane_now();
     if (row >= P.M) return;
     const_u32* xc = (const_u32*)(P.x);
 #pragma unroll
@@ -593,8 +606,8 @@ void gemv_kernel(const GemvGroup grp) {
         float sum[B];
         run_piece<B>(P, pc, L, sum);
         if (c == 0 && c1 == P.nblk) {
-            const RowTail rt = load_rows(P, t, lane);
-            store_rows<B>(P, t, lane, sum, rt);
+            const RowTail rt = load_rows(P, t);
+            store_rows<B>(P, t, sum, rt);
         } else {
             const uint32_t t0 = P.blk_base + static_cast<uint32_t>(t) * P.nblk;
             const int wa = __builtin_amdgcn_readfirstlane(wave_of(t0, grp));
@@ -604,29 +617,30 @@ void gemv_kernel(const GemvGroup grp) {
             const int slot_wa = __builtin_amdgcn_readfirstlane(range_begin(wa, grp) >= t0 ? 0 : 1);
             auto slot_of = [&](int v) { return v > wa ? 0 : slot_wa; };
             const int a = max(wa, w0), b = min(wb, wlast);
-            float* mine = s_piece + (wid * 2 + (first ? 0 : 1)) * B * 64 + lane;
+            const int ln = lane_now();
+            float* mine = s_piece + (wid * 2 + (first ? 0 : 1)) * B * 64 + ln;
 #pragma unroll
             for (int bb = 0; bb < B; ++bb) mine[bb * 64] = sum[bb];
             // LDS operations of a wave complete in order, and the last wave reads the
             // pieces only after its own count: no fence is needed
             uint32_t arrived = 0;
-            if (lane == 0)
+            if (ln == 0)
                 arrived = __hip_atomic_fetch_add(s_cnt + 2 * (b - w0) + slot_of(b), 1u, __ATOMIC_RELAXED,
                                                  __HIP_MEMORY_SCOPE_WORKGROUP);
             arrived = __builtin_amdgcn_readfirstlane(arrived);
             if (arrived == static_cast<uint32_t>(b - a)) {
                 // last of this workgroup's pieces of the tile: add them in wave order
-                const RowTail rt = load_rows(P, t, lane);   // in flight while the sums combine
+                const RowTail rt = load_rows(P, t);   // in flight while the sums combine
                 float tot[B];
 #pragma unroll
                 for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
                 for (int v = a; v <= b; ++v) {
-                    const float* pv = s_piece + ((v - w0) * 2 + slot_of(v)) * B * 64 + lane;
+                    const float* pv = s_piece + ((v - w0) * 2 + slot_of(v)) * B * 64 + ln;
 #pragma unroll
                     for (int bb = 0; bb < B; ++bb) tot[bb] += pv[bb * 64];
                 }
                 if (wa >= w0 && wb <= wlast) {
-                    store_rows<B>(P, t, lane, tot, rt);
+                    store_rows<B>(P, t, tot, rt);
                 } else {
                     // the tile reaches into other workgroups: publish this workgroup's sum.
                     // Workgroup sums and counters are accessed only with device-scope
@@ -636,13 +650,13 @@ void gemv_kernel(const GemvGroup grp) {
                     const int gslot_ga =
                         __builtin_amdgcn_readfirstlane(range_begin(ga * kGemvWaves, grp) >= t0 ? 0 : 1);
                     auto gslot_of = [&](int h) { return h > ga ? 0 : gslot_ga; };
-                    float* gp = grp.partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + lane;
+                    float* gp = grp.partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + ln;
 #pragma unroll
                     for (int bb = 0; bb < B; ++bb)
                         __hip_atomic_store(gp + bb * 64, tot[bb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
                     uint32_t garr = 0;
-                    if (lane == 0)
+                    if (ln == 0)
                         garr = __hip_atomic_fetch_add(grp.counters + gb, 1u, __ATOMIC_RELAXED,
                                                       __HIP_MEMORY_SCOPE_AGENT);
                     garr = __builtin_amdgcn_readfirstlane(garr);
@@ -657,7 +671,7 @@ void gemv_kernel(const GemvGroup grp) {
                                 const int h = h0 + u;
                                 if (h <= gb) {
                                     const float* ph =
-                                        grp.partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + lane;
+                                        grp.partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + ln;
 #pragma unroll
                                     for (int bb = 0; bb < B; ++bb)
                                         pv[u][bb] = __hip_atomic_load(ph + bb * 64, __ATOMIC_RELAXED,
@@ -671,9 +685,9 @@ void gemv_kernel(const GemvGroup grp) {
                                     for (int bb = 0; bb < B; ++bb) tot[bb] += pv[u][bb];
                                 }
                         }
-                        if (lane == 0)
+                        if (ln == 0)
                             __hip_atomic_store(grp.counters + gb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        store_rows<B>(P, t, lane, tot, rt);
+                        store_rows<B>(P, t, tot, rt);
                     }
                 }
             }
