@@ -105,8 +105,10 @@ size_t tetra_tail_offset(int M, int K);
  *   - block columns 4g..4g+3 (g < ng) form a 1536-byte run at g*1536: the
  *     32-bit part of column 4g+k of row r at 16*r + 4*k, its 16-bit part at
  *     1024 + 8*r + 2*k (one 16-byte and one 8-byte load per row and group);
- *   - each remaining column b = 4*ng + q (q < nblk mod 4) is a 384-byte run
- *     at ng*1536 + q*384: 32-bit part at 4*r, 16-bit part at 256 + 2*r.
+ *   - the s = nblk mod 4 remaining columns b = 4*ng + q (q < s) form one
+ *     run of 384*s bytes at ng*1536: 32-bit part at 4*s*r + 4*q; 16-bit
+ *     part at 256*s + 2*min(s,2)*r + 2*q for q < 2, and at 1024 + 2*r for
+ *     q = 2 (a row reads its remaining words with whole loads).
  * Each word is stored recoded, still 48 bits and one-to-one
  * with the canonical word: path = s8 | b1<<6 | b2<<7 | b3<<11, g, the
  * physical rank-table row of section 1, i2, and section 3's physical row

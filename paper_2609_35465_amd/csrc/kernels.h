@@ -106,6 +106,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint16_t* __restrict_
 
 typedef __attribute__((address_space(3))) const uint32_t lds_u32;
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
 typedef __attribute__((address_space(3))) const u32x2 lds_u2;
 typedef __attribute__((address_space(3))) const float lds_f32;
 typedef __attribute__((address_space(3))) const uint8_t lds_bytes;
@@ -168,7 +169,9 @@ __device__ __forceinline__ uint32_t block_values(const BlockFetch& f, uint32_t y
 }
 
 // Decoder tables into LDS: all loads first, then all stores, so that a
-// workgroup pays one memory round trip (NT: threads of the workgroup).
+// workgroup pays one memory round trip (NT: threads of the workgroup).  The
+// loads and stores are unconditional, so that none is sunk into a branch: a
+// thread past the end loads and stores the last word again.
 template <int NT>
 struct TableStage {
     static constexpr int kN = static_cast<int>(kPackedTableBytes / 16);
@@ -181,10 +184,7 @@ struct TableStage {
     }
     __device__ __forceinline__ void store(uint4* dst) const {
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int i = static_cast<int>(threadIdx.x) + k * NT;
-            if (i < kN) dst[i] = v[k];
-        }
+        for (int k = 0; k < kPer; ++k) dst[min(static_cast<int>(threadIdx.x) + k * NT, kN - 1)] = v[k];
     }
 };
 
@@ -276,8 +276,8 @@ struct GemvGroup {
     GemvProblem prob[kMaxGroup];
     double inv_total, inv_waves;   // 1 / total, 1 / waves
     uint32_t total;                // blocks in the launch sequence (< 2^31)
-    uint32_t* counters;            // [W / 16], zero between launches
-    float* partials;               // [W / 16][2][B][64]
+    uint32_t* counters;            // [groups], zero between launches
+    float* partials;               // [groups][2][B][64]
     int n, waves;
 };
 
@@ -423,38 +423,51 @@ __device__ __forceinline__ void run_item(Pipe<B>& st, const ItemWords& cw, const
     }
 }
 
-__device__ __forceinline__ ItemWords load_item(const uint8_t* tb, int j, int ng, int rem, int lane) {
+// code words of group j of a tile (four columns)
+__device__ __forceinline__ ItemWords load_group(const uint8_t* tb, int j, int lane) {
     ItemWords w;
-    if (j < ng) {
-        const uint8_t* gp = tb + static_cast<size_t>(j) * tetra::kGroupBytes;
-        w.lo = *reinterpret_cast<const uint4*>(gp + 16 * lane);
-        w.hi = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * lane);
-    } else {
-        // the nblk mod 4 single columns, 384-byte runs
-        const uint8_t* sp = tb + static_cast<size_t>(ng) * tetra::kGroupBytes;
-        lane = lane_now();
-        w.lo = make_uint4(0, 0, 0, 0);
+    const uint8_t* gp = tb + static_cast<size_t>(j) * tetra::kGroupBytes;
+    w.lo = *reinterpret_cast<const uint4*>(gp + 16 * lane);
+    w.hi = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * lane);
+    return w;
+}
+
+// code words of the rem = nblk mod 4 trailing columns of a tile (rem > 0),
+// whole loads straight into the item registers; the words of columns past
+// rem are left unset and never read
+__device__ __forceinline__ ItemWords load_trailing(const uint8_t* tb, int ng, int rem) {
+    const uint8_t* sp = tb + static_cast<size_t>(ng) * tetra::kGroupBytes;
+    const int lane = lane_now();
+    ItemWords w;
+    if (rem == 1) {
         w.lo.x = *reinterpret_cast<const uint32_t*>(sp + 4 * lane);
-        uint32_t h0 = *reinterpret_cast<const uint16_t*>(sp + 256 + 2 * lane), h1 = 0, h2 = 0;
-        if (rem > 1) {
-            w.lo.y = *reinterpret_cast<const uint32_t*>(sp + kChunk + 4 * lane);
-            h1 = *reinterpret_cast<const uint16_t*>(sp + kChunk + 256 + 2 * lane);
-        }
-        if (rem > 2) {
-            w.lo.z = *reinterpret_cast<const uint32_t*>(sp + 2 * kChunk + 4 * lane);
-            h2 = *reinterpret_cast<const uint16_t*>(sp + 2 * kChunk + 256 + 2 * lane);
-        }
-        w.hi = make_uint2(h0 | h1 << 16, h2);
+        w.hi.x = *reinterpret_cast<const uint16_t*>(sp + 256 + 2 * lane);
+    } else if (rem == 2) {
+        const u32x2 l = *reinterpret_cast<const u32x2*>(sp + 8 * lane);
+        w.lo.x = l.x;
+        w.lo.y = l.y;
+        w.hi.x = *reinterpret_cast<const uint32_t*>(sp + 512 + 4 * lane);
+    } else {
+        const u32x3 l = *reinterpret_cast<const u32x3*>(sp + 12 * lane);
+        w.lo.x = l.x;
+        w.lo.y = l.y;
+        w.lo.z = l.z;
+        w.hi.x = *reinterpret_cast<const uint32_t*>(sp + 768 + 4 * lane);
+        w.hi.y = *reinterpret_cast<const uint16_t*>(sp + 1024 + 2 * lane);
     }
     return w;
 }
 
-// A piece of a tile: block columns c0..c1-1 of tile t.  begin_piece issues
-// the loads of its first two items, so that they can be in flight while the
-// workgroup stages its tables; run_piece sums the piece for the wave's 64 rows.
+// A piece of a tile: block columns c0..c1-1 of tile t, in groups j..jg and,
+// when the piece reaches them (tr), the trailing columns.  begin_piece issues
+// the loads of its first two groups and of its trailing columns, so that all
+// of them are in flight together; run_piece sums the piece for the wave's 64
+// rows, the trailing columns after the groups, from their own registers (in
+// the group pipeline, their loads would make it wait).
 struct Piece {
-    ItemWords cw, nw;
-    int t, c0, c1, j, j1;
+    ItemWords cw, nw, tw;
+    int t, c0, c1, j, jg;
+    bool tr;
 };
 
 __device__ __forceinline__ Piece begin_piece(const GemvProblem& P, int t, int c0, int c1, int lane) {
@@ -462,68 +475,90 @@ __device__ __forceinline__ Piece begin_piece(const GemvProblem& P, int t, int c0
     pc.t = t;
     pc.c0 = c0;
     pc.c1 = c1;
-    pc.j = min(c0 >> 2, P.ng);
-    pc.j1 = min((c1 - 1) >> 2, P.ng);
+    pc.j = c0 >> 2;                                  // ng when the piece starts in the trailing columns
+    pc.jg = min((c1 - 1) >> 2, P.ng - 1);            // last group of the piece (< j: none)
+    pc.tr = c1 > 4 * P.ng;
     const uint8_t* tb = P.codes + static_cast<size_t>(t) * P.nblk * kChunk;
-    pc.cw = load_item(tb, pc.j, P.ng, P.rem, lane);
-    pc.nw = load_item(tb, min(pc.j + 1, pc.j1), P.ng, P.rem, lane);
+    if (pc.j <= pc.jg) {
+        pc.cw = load_group(tb, pc.j, lane);
+        pc.nw = load_group(tb, min(pc.j + 1, pc.jg), lane);
+    }
+    if (pc.tr) pc.tw = load_trailing(tb, P.ng, P.rem);
     return pc;
 }
 
-// blocks of item j whose words are in cw (next item's words in nw)
+// blocks kb..ke-1 of item j (words cw; the next item's words nw, column
+// ncol0), whole group or not
 template <int B>
-__device__ __forceinline__ void run_one_item(Pipe<B>& st, const GemvProblem& P, const Piece& pc, int j, int kb,
+__device__ __forceinline__ void run_one_item(Pipe<B>& st, int kb, int ke, int col0, int ncol0,
                                              const ItemWords& cw, const ItemWords& nw, lds_bytes* L,
                                              const_u32* xc, int kp) {
-    const int ke = __builtin_amdgcn_readfirstlane(j == pc.j1 ? pc.c1 - 4 * j : (j < P.ng ? tetra::kGroupCols : P.rem));
-    const int col0 = __builtin_amdgcn_readfirstlane(4 * j);
-    const int ncol0 = __builtin_amdgcn_readfirstlane(4 * min(j + 1, pc.j1));
     if (kb == 0 && ke == tetra::kGroupCols)
         run_item<B, true>(st, cw, nw, col0, ncol0, 0, tetra::kGroupCols, L, xc, kp);
     else
         run_item<B, false>(st, cw, nw, col0, ncol0, kb, ke, L, xc, kp);
 }
 
-// The items alternate between two sets of word registers, so that the loads
-// of the item after next go straight into the registers just freed.
+// first block of a run of items: its table reads and activations, and an
+// empty "previous block"
+template <int B>
+__device__ __forceinline__ void start_pipe(Pipe<B>& st, const ItemWords& w, int kb, int col, lds_bytes* L,
+                                           const_u32* xc, int kp) {
+    uint32_t lo, hi;
+    if (kb == 0) block_word<0>(w, lo, hi);
+    else if (kb == 1) block_word<1>(w, lo, hi);
+    else if (kb == 2) block_word<2>(w, lo, hi);
+    else block_word<3>(w, lo, hi);
+    st.cur = fetch_block(lo, hi, L);
+    load_x<B>(st.x, xc, kp, col);
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    st.ps = 0.f;
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) st.pdt[bb] = 0.f;
+}
+
+// The groups alternate between two sets of word registers, so that the
+// loads of the group after next go straight into the registers just freed;
+// the trailing columns follow from their own registers.
 template <int B>
 __device__ __forceinline__ void run_piece(const GemvProblem& P, Piece& pc, lds_bytes* L, float (&out)[B]) {
-    const int ng = P.ng;
     const int lane = threadIdx.x & 63;
     const uint8_t* tb = P.codes + static_cast<size_t>(pc.t) * P.nblk * kChunk;
     const_u32* xc = (const_u32*)(P.x);
     const int kp = P.K >> 1;
-    const int j1 = pc.j1;
+    const int jg = pc.jg;
     int j = pc.j;
     int kb = pc.c0 - 4 * j;
     Pipe<B> st;
-    {
-        uint32_t lo, hi;
-        if (kb == 0) block_word<0>(pc.cw, lo, hi);
-        else if (kb == 1) block_word<1>(pc.cw, lo, hi);
-        else if (kb == 2) block_word<2>(pc.cw, lo, hi);
-        else block_word<3>(pc.cw, lo, hi);
-        st.cur = fetch_block(lo, hi, L);
-        load_x<B>(st.x, xc, kp, pc.c0);
-        __builtin_amdgcn_s_waitcnt(0xC07F);
-    }
 #pragma unroll
-    for (int bb = 0; bb < B; ++bb) st.acc[bb] = st.pdt[bb] = 0.f;
-    st.ps = 0.f;
-    ItemWords wa = pc.cw, wb = pc.nw;
-    for (;;) {
-        run_one_item<B>(st, P, pc, j, kb, wa, wb, L, xc, kp);
-        if (j == j1) break;
-        ++j;
+    for (int bb = 0; bb < B; ++bb) st.acc[bb] = 0.f;
+    if (j <= jg) {
+        // the last group ends the piece unless the trailing columns follow
+        const int kl = __builtin_amdgcn_readfirstlane(pc.tr ? tetra::kGroupCols : pc.c1 - 4 * jg);
+        start_pipe<B>(st, pc.cw, kb, pc.c0, L, xc, kp);
+        ItemWords wa = pc.cw, wb = pc.nw;
+        for (;;) {
+            run_one_item<B>(st, kb, j == jg ? kl : tetra::kGroupCols, 4 * j, 4 * min(j + 1, jg), wa, wb, L, xc, kp);
+            if (j == jg) break;
+            ++j;
+            kb = 0;
+            wa = load_group(tb, min(j + 1, jg), lane);
+            run_one_item<B>(st, 0, j == jg ? kl : tetra::kGroupCols, 4 * j, 4 * min(j + 1, jg), wb, wa, L, xc, kp);
+            if (j == jg) break;
+            ++j;
+            wb = load_group(tb, min(j + 1, jg), lane);
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        finish_pending<B>(st);
         kb = 0;
-        wa = load_item(tb, min(j + 1, j1), ng, P.rem, lane);
-        run_one_item<B>(st, P, pc, j, 0, wb, wa, L, xc, kp);
-        if (j == j1) break;
-        ++j;
-        wb = load_item(tb, min(j + 1, j1), ng, P.rem, lane);
     }
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    finish_pending<B>(st);
+    if (pc.tr) {
+        const int c = 4 * P.ng;
+        start_pipe<B>(st, pc.tw, kb, c + kb, L, xc, kp);
+        run_item<B, false>(st, pc.tw, pc.tw, c, c, kb, pc.c1 - c, L, xc, kp);
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        finish_pending<B>(st);
+    }
 #pragma unroll
     for (int bb = 0; bb < B; ++bb) out[bb] = st.acc[bb];
 }

@@ -105,8 +105,11 @@ __host__ __device__ inline uint64_t canonical_from_device(DeviceWord d) {
 // Block columns go in groups of four: group g is a 1536-byte run holding, for
 // lane (row in tile) r, the 32-bit parts of columns 4g..4g+3 at 16r and
 // their 16-bit parts at 1024 + 8r, so a lane reads a group with one 16-byte
-// and one 8-byte load.  The nblk mod 4 trailing columns follow as 384-byte
-// runs: 32-bit parts at 4r, 16-bit parts at 256 + 2r.
+// and one 8-byte load.  The s = nblk mod 4 trailing columns follow as one
+// run of 384 s bytes, laid out so that a lane reads them with whole loads and
+// no bit assembly: the 32-bit parts of lane r at 4 s r (columns in order);
+// the 16-bit parts of the first two columns at 256 s + 2 min(s, 2) r, and
+// that of a third column at 1024 + 2r.
 constexpr int kGroupCols = 4;
 constexpr int kGroupBytes = 1536;
 constexpr int kColBytes = 384;
@@ -123,9 +126,11 @@ __host__ __device__ inline WordLoc word_loc(int nblk, int r, int b) {
         w.lo_off = static_cast<uint32_t>(g * kGroupBytes + 16 * r + 4 * k);
         w.hi_off = static_cast<uint32_t>(g * kGroupBytes + 1024 + 8 * r + 2 * k);
     } else {
-        const int base = ng * kGroupBytes + (b - ng * kGroupCols) * kColBytes;
-        w.lo_off = static_cast<uint32_t>(base + 4 * r);
-        w.hi_off = static_cast<uint32_t>(base + 256 + 2 * r);
+        const int s = nblk - ng * kGroupCols, k = b - ng * kGroupCols;
+        const int base = ng * kGroupBytes;
+        w.lo_off = static_cast<uint32_t>(base + 4 * s * r + 4 * k);
+        w.hi_off = static_cast<uint32_t>(k < 2 ? base + 256 * s + 2 * (s < 2 ? s : 2) * r + 2 * k
+                                               : base + 1024 + 2 * r);
     }
     return w;
 }

@@ -89,14 +89,16 @@ def _stored_word(blob, nblk, tile, r, b):
         lo_at = base + g * 1536 + 16 * r + 4 * k
         hi_at = base + g * 1536 + 1024 + 8 * r + 2 * k
     else:
-        run = base + ng * 1536 + (b - 4 * ng) * 384
-        lo_at, hi_at = run + 4 * r, run + 256 + 2 * r
+        s, q = nblk - 4 * ng, b - 4 * ng
+        run = base + ng * 1536
+        lo_at = run + 4 * s * r + 4 * q
+        hi_at = run + 256 * s + 2 * min(s, 2) * r + 2 * q if q < 2 else run + 1024 + 2 * r
     lo = int(blob[lo_at:lo_at + 4].view(np.uint32)[0])
     hi = int(blob[hi_at:hi_at + 2].view(np.uint16)[0])
     return lo, hi
 
 
-@pytest.mark.parametrize("nblk,T", [(3, 16), (9, 6), (8, 0)])
+@pytest.mark.parametrize("nblk,T", [(3, 16), (9, 6), (8, 0), (6, 2), (7, 10), (2, 0), (1, 4)])
 def test_pack_layout_is_the_documented_chunking(nblk, T):
     M, K = 70, 24 * nblk + T
     rng = np.random.default_rng(3 + nblk)
