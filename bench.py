@@ -52,10 +52,11 @@ def parse():
                     help="matrix: one launch per matrix; deps: per layer [q,k,v] [o] "
                          "[gate,up] [down] (the launches a decode step can fuse); "
                          "layer: one grouped launch per layer")
-    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4"],
+    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4", "head"],
                     help="tetra: every projection a Tetra matrix (the GEMV metric); c4: the "
                          "full decode step -- 10%% of the projections (seeded) stored as int4 "
-                         "w4g128 and one 4-bit embedding row gathered per step")
+                         "w4g128 and one 4-bit embedding row gathered per step; head: the "
+                         "4-bit output head GEMV (151936 x 5120, groups of 64) alone")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the benchmark: copy a buffer of this many MiB five "
                          "times with torch (a plain copy kernel of known size, the "
@@ -291,6 +292,106 @@ def recorded_traffic(args, layers):
         return None
 
 
+HEAD_ROWS, HEAD_DIM = 151936, 5120
+
+
+def main_head(args, torch, tt):
+    """The 4-bit output head (151,936 x 5,120, groups of 64): one
+    tetra_head4_gemv launch per step, alternating between two copies of the
+    table (876 MB together, more than the last-level cache) so that every
+    launch streams from HBM."""
+    from oracle import int4 as oint4
+    rows, dim, B = HEAD_ROWS, HEAD_DIM, args.batch
+    gen = torch.Generator(device="cuda").manual_seed(0x7E7A_0000 + 0x50)
+    tables = []
+    for _ in range(2):
+        q = torch.empty((rows, dim // 2), dtype=torch.uint8, device="cuda").random_(0, 256, generator=gen)
+        sc = (torch.rand((rows, dim // 64), generator=gen, device="cuda") * 1.5 + 0.5) * (1e-2 / 8)
+        tables.append((q, torch.stack([sc, -7.5 * sc], dim=-1).half().contiguous()))
+    from paper_2609_35465_amd import workloads
+    x = torch.as_tensor(workloads.activations(0x7E7A_0050, B, dim)).cuda()
+    ys = [torch.empty((B, rows), dtype=torch.float32, device="cuda") for _ in tables]
+    stream = torch.cuda.current_stream()
+
+    def step_pair(s=None):
+        st = (s or stream).cuda_stream
+        for (q, so), y in zip(tables, ys):
+            tt.head4_gemv(q, so, x, y, rows, dim, B, stream=st)
+
+    for _ in range(max(1, args.warmup)):
+        step_pair()
+    torch.cuda.synchronize()
+    # parity: sampled rows of both tables against the oracle
+    sample = np.unique(np.r_[0:8, rows - 8:rows, np.linspace(0, rows - 1, 48).astype(int)])
+    idx = torch.as_tensor(sample, device="cuda")
+    worst = 0.0
+    for (q, so), y in zip(tables, ys):
+        ref, norm = oint4.int4_gemv_f64(q[idx].cpu().numpy(), so[idx].cpu().numpy(), x.cpu().numpy(), group=64)
+        got = y.cpu().numpy()[:, sample].astype(np.float64)
+        worst = max(worst, float((np.abs(got - ref) / norm).max()))
+    graph = None
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step_pair(torch.cuda.current_stream())
+        ref = [y.clone() for y in ys]
+        for _ in range(3):
+            for y in ys:
+                y.zero_()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert all(torch.equal(r, y) for r, y in zip(ref, ys)), "graph replay differs from the eager run"
+    run = graph.replay if graph is not None else step_pair
+    pairs = max(1, args.steps // 2)
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(pairs):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / (2 * pairs)
+    read_bytes = rows * dim // 2 + rows * (dim // 64) * 4
+    algo = read_bytes + 2 * dim * B + 4 * rows * B
+    value = algo / (ms_step * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": 2 * pairs,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16-in/f32-acc", "data": "synthetic",
+        "config": {"workload": f"4-bit output head {rows} x {dim}, groups of 64, batch {B}, "
+                               "two tables alternating", "batch": B, "hip_graph": graph is not None},
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "bits_read_per_weight": round(read_bytes * 8 / (rows * dim), 4),
+        "weights_per_s": round(rows * dim / (ms_step * 1e-3), 1),
+        "parity_head4_worst_rel_err": worst,
+        "roofline": {"bound": "hbm", "achieved": round(value, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(value / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "int4_gemv_kernel (groups of 64)", "avg_launch_us": round(ms_step * 1e3, 3),
+                     "bytes_per_launch": algo},
+    }
+    if not args.no_cpu_baseline:
+        # the oracle on 2048-row slices of the first table until the time is used
+        q, so = tables[0]
+        xh = x.cpu().numpy()
+        t_used, done = 0.0, 0
+        for r0 in range(0, rows, 2048):
+            if t_used >= args.cpu_seconds:
+                break
+            qs, ss = q[r0:r0 + 2048].cpu().numpy(), so[r0:r0 + 2048].cpu().numpy()
+            t0 = time.perf_counter()
+            oint4.int4_gemv_f64(qs, ss, xh, group=64)
+            t_used += time.perf_counter() - t0
+            done += len(qs)
+        out["cpu_baseline"] = {
+            "value": round(done * (dim // 2 + (dim // 64) * 4) / t_used / 1e9, 6), "unit": "GB/s",
+            "cores": 1, "kind": "oracle",
+            "sample": f"{done} rows of the head in {t_used:.1f} s, float64 numpy, batch {B}"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -313,6 +414,8 @@ def main():
         assert torch.equal(src, dst)
         print(json.dumps({"copy_probe_bytes": n, "copies": 5}), flush=True)
         return 0
+    if args.workload == "head":
+        return main_head(args, torch, tt)
     stream = torch.cuda.current_stream()
     plan, L, emb = build_workload(torch, tt, args.model, args.layers, args.batch, args.workload)
     torch.cuda.synchronize()

@@ -211,6 +211,22 @@ int tetra_int4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x,
                     int batch, hipStream_t stream);
 
 /*
+ * The 4-bit output head (Sec. 4.4): a table of `rows` outputs by `dim`
+ * inputs in the embedding layout (groups of 64 along dim, fp16 scale and
+ * offset per group, nibbles as in tetra_int4_gemv), times the activations:
+ *   y[b][r] = sum_k (scale[r][k/64] * q[r][k] + offset[r][k/64]) * x[b][k]
+ *   q:         device bytes [rows][dim/2], 8-byte aligned
+ *   scale_off: device fp16 [rows][dim/64][2], 4-byte aligned
+ *   x:         device fp16 [batch][dim], 16-byte aligned
+ *   y:         device fp32 [batch][rows], fully overwritten
+ * dim must be a positive multiple of 64; batch 1..TETRA_MAX_BATCH.
+ * Deterministic and batch-invariant.  Asynchronous; TETRA_EINVAL /
+ * TETRA_EALIGN / TETRA_EDEVICE as for tetra_gemv.
+ */
+int tetra_head4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x, float* y, int rows, int dim,
+                     int batch, hipStream_t stream);
+
+/*
  * Rows of a 4-bit embedding table (Sec. 4.4): groups of 64 along the
  * embedding dimension, fp16 scale and offset per group, nibbles as in
  * tetra_int4_gemv;  out[i][k] = fl32(fl32(scale * q) + offset) for the row

@@ -36,6 +36,7 @@ _SIGNATURES = {
     "tetra_decode": (_int, [_vp, _sz, _vp, _vp, _vp]),
     "tetra_dequant": (_int, [_vp, _vp, _int, _int, _vp, _vp]),
     "tetra_int4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
+    "tetra_head4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_emb4_gather": (_int, [_vp, _vp, _int, _int, _vp, _int, _vp, _vp]),
 }
 EXPORTED = tuple(_SIGNATURES)
@@ -175,6 +176,13 @@ def int4_gemv(q, scale_off, x, y, M: int, K: int, batch: int = 1, stream=None):
     [M, K/128, 2], x fp16 [batch, K] (all device tensors)."""
     _check(_call("tetra_int4_gemv", _ptr(q), _ptr(scale_off), _ptr(x), _ptr(y), M, K, batch,
                  _stream(stream)), "tetra_int4_gemv")
+
+
+def head4_gemv(q, scale_off, x, y, rows: int, dim: int, batch: int = 1, stream=None):
+    """y[batch, rows] for the 4-bit output head: q uint8 [rows, dim/2],
+    scale_off fp16 [rows, dim/64, 2], x fp16 [batch, dim] (device tensors)."""
+    _check(_call("tetra_head4_gemv", _ptr(q), _ptr(scale_off), _ptr(x), _ptr(y), rows, dim, batch,
+                 _stream(stream)), "tetra_head4_gemv")
 
 
 def emb4_gather(q, scale_off, rows: int, dim: int, tokens, out, stream=None):

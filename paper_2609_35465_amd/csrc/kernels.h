@@ -744,25 +744,28 @@ void gemv_kernel(const GemvGroup grp) {
 // ----------------------------------------------------- int4 projections
 //
 // The int4 records of a served file (Sec. 4.1, Sec. 4.3): 4-bit weights in
-// groups of 128 along K with an fp16 scale and offset per group,
+// groups of G = 128 along K with an fp16 scale and offset per group,
 // w = scale * q + offset, q the unsigned nibble (element 2i in the low
-// nibble of byte i).  Per group the product is
+// nibble of byte i).  The 4-bit output head (Sec. 4.4) has the same form
+// with G = 64.  Per group the product is
 //   sum_k w_k x_k = scale * sum_k q_k x_k + offset * sum_k x_k,
 // so the nibbles go to fp16 unscaled and the group's scale and offset are
-// applied once.
+// applied once per lane and group.
 //
-// Layout: q [M][K/2] bytes, scale/offset [M][K/128][2] fp16, both row-major.
-// A wave takes 4 rows at a time and walks K in steps of 1024 weights, 16 per
-// lane (8 bytes of q per row, coalesced into 512-byte runs); the lane's 16
-// activations are loaded once per step for the 4 rows.  Nibble k of a dword
-// and nibble k+4 become one fp16 pair with a single and-or against the bits
-// of 1024.0 (giving 1024 + q exactly); the activation pairs are permuted to
-// match, and 1024 times the lane's activation sum is taken back out.  Lanes
-// are added with a fixed butterfly, so results are deterministic and
-// batch-invariant.
+// Layout: q [M][K/2] bytes, scale/offset [M][K/G][2] fp16, both row-major.
+// A wave takes 2 rows and walks K in steps of 1024 weights, 16 per lane (8
+// bytes of q per row, coalesced into 512-byte runs); two steps are loaded
+// before either is used, so that a wave keeps 2 KB of q in flight.  Few rows
+// per wave give many waves, which is what hides the memory latency (4 rows
+// per wave ran 1.4-2.5x slower).  Nibble k of a dword and nibble k+4 become
+// one fp16 pair with a single and-or against the bits of 1024.0 (giving
+// 1024 + q exactly); the activation pairs are permuted to match, and 1024
+// times the lane's activation sum is taken back out.  Lanes are added with a
+// fixed butterfly, so results are deterministic and batch-invariant.
 
 constexpr int kInt4Group = 128;
-constexpr int kInt4RowsPerWave = 4;
+constexpr int kHead4Group = 64;
+constexpr int kInt4RowsPerWave = 2;
 constexpr int kInt4Waves = 4;
 
 __device__ __forceinline__ float wave_sum(float v) {
@@ -771,7 +774,79 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// one lane's 16 activations of batch row b at k0, paired (k, k+4) within each
+// 8 to match the nibble pairs, and their sum
 template <int B>
+struct Int4X {
+    uint32_t xp[B][8];
+    float sx[B];
+};
+
+template <int B>
+__device__ __forceinline__ void int4_load_x(Int4X<B>& a, const uint16_t* __restrict__ x, int K, int k0) {
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) {
+        const uint4* xs = reinterpret_cast<const uint4*>(x + static_cast<size_t>(bb) * K + k0);
+        const uint4 u = xs[0], v = xs[1];
+        const uint32_t n[8] = {u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w};   // pairs (2i, 2i+1)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            // elements 8h..8h+7: natural pairs n[4h..4h+3]; wanted (e, e+4) for e = 0..3
+            a.xp[bb][4 * h + 0] = __builtin_amdgcn_perm(n[4 * h + 2], n[4 * h + 0], 0x05040100u);
+            a.xp[bb][4 * h + 1] = __builtin_amdgcn_perm(n[4 * h + 2], n[4 * h + 0], 0x07060302u);
+            a.xp[bb][4 * h + 2] = __builtin_amdgcn_perm(n[4 * h + 3], n[4 * h + 1], 0x05040100u);
+            a.xp[bb][4 * h + 3] = __builtin_amdgcn_perm(n[4 * h + 3], n[4 * h + 1], 0x07060302u);
+        }
+        float sacc = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sacc = dot2(n[i], 0x3C003C00u, sacc);
+        a.sx[bb] = sacc;
+    }
+}
+
+// the rows' q words and group scale/offset at k0
+struct Int4W {
+    uint2 w[kInt4RowsPerWave];
+    uint32_t so[kInt4RowsPerWave];
+};
+
+template <int G>
+__device__ __forceinline__ void int4_load_w(Int4W& a, const uint8_t* __restrict__ q, const uint16_t* __restrict__ so,
+                                            int M, int K, int r0, int k0) {
+    const int groups = K / G;
+#pragma unroll
+    for (int r = 0; r < kInt4RowsPerWave; ++r) {
+        const int row = min(r0 + r, M - 1);
+        a.w[r] = *reinterpret_cast<const uint2*>(q + static_cast<size_t>(row) * (K >> 1) + (k0 >> 1));
+        a.so[r] = *reinterpret_cast<const uint32_t*>(so + (static_cast<size_t>(row) * groups + k0 / G) * 2);
+    }
+}
+
+template <int B>
+__device__ __forceinline__ void int4_step(float (&acc)[kInt4RowsPerWave][B], const Int4W& a, const Int4X<B>& xa) {
+#pragma unroll
+    for (int r = 0; r < kInt4RowsPerWave; ++r) {
+        const float sc = f16(static_cast<uint16_t>(a.so[r])), of = f16(static_cast<uint16_t>(a.so[r] >> 16));
+        uint32_t np[8];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const uint32_t d = h ? a.w[r].y : a.w[r].x;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                np[4 * h + e] = ((d >> (4 * e)) & 0x000F000Fu) | 0x64006400u;   // (1024 + q_e, 1024 + q_{e+4})
+        }
+#pragma unroll
+        for (int bb = 0; bb < B; ++bb) {
+            float dt = 0.f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) dt = dot2(np[i], xa.xp[bb][i], dt);
+            // sum q x = dt - 1024 sx; times scale, plus offset * sx
+            acc[r][bb] = fmaf(sc, fmaf(-1024.f, xa.sx[bb], dt), fmaf(of, xa.sx[bb], acc[r][bb]));
+        }
+    }
+}
+
+template <int B, int G>
 __global__ __launch_bounds__(kInt4Waves * 64) void int4_gemv_kernel(const uint8_t* __restrict__ q,
                                                                    const uint16_t* __restrict__ so,
                                                                    const uint16_t* __restrict__ x,
@@ -780,58 +855,24 @@ __global__ __launch_bounds__(kInt4Waves * 64) void int4_gemv_kernel(const uint8_
     const int wave = blockIdx.x * kInt4Waves + (threadIdx.x >> 6);
     const int r0 = wave * kInt4RowsPerWave;
     if (r0 >= M) return;
-    const int groups = K / kInt4Group;
     float acc[kInt4RowsPerWave][B];
 #pragma unroll
     for (int r = 0; r < kInt4RowsPerWave; ++r)
 #pragma unroll
         for (int bb = 0; bb < B; ++bb) acc[r][bb] = 0.f;
-    for (int k0 = 16 * lane; k0 < K; k0 += 1024) {
-        // activations of this lane's 16 weights, paired (k, k+4) within each 8
-        uint32_t xp[B][8];
-        float sx[B];
-#pragma unroll
-        for (int bb = 0; bb < B; ++bb) {
-            const uint4* xs = reinterpret_cast<const uint4*>(x + static_cast<size_t>(bb) * K + k0);
-            const uint4 a = xs[0], b = xs[1];
-            const uint32_t n[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};   // pairs (2i, 2i+1)
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                // elements 8h..8h+7: natural pairs n[4h..4h+3]; wanted (e, e+4) for e = 0..3
-                xp[bb][4 * h + 0] = __builtin_amdgcn_perm(n[4 * h + 2], n[4 * h + 0], 0x05040100u);
-                xp[bb][4 * h + 1] = __builtin_amdgcn_perm(n[4 * h + 2], n[4 * h + 0], 0x07060302u);
-                xp[bb][4 * h + 2] = __builtin_amdgcn_perm(n[4 * h + 3], n[4 * h + 1], 0x05040100u);
-                xp[bb][4 * h + 3] = __builtin_amdgcn_perm(n[4 * h + 3], n[4 * h + 1], 0x07060302u);
-            }
-            float s = 0.f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) s = dot2(n[i], 0x3C003C00u, s);
-            sx[bb] = s;
-        }
-        const int g = k0 / kInt4Group;
-#pragma unroll
-        for (int r = 0; r < kInt4RowsPerWave; ++r) {
-            const int row = min(r0 + r, M - 1);
-            const uint2 w = *reinterpret_cast<const uint2*>(q + static_cast<size_t>(row) * (K >> 1) + (k0 >> 1));
-            const uint32_t sov = *reinterpret_cast<const uint32_t*>(so + (static_cast<size_t>(row) * groups + g) * 2);
-            const float sc = f16(static_cast<uint16_t>(sov)), of = f16(static_cast<uint16_t>(sov >> 16));
-            uint32_t np[8];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const uint32_t d = h ? w.y : w.x;
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    np[4 * h + e] = ((d >> (4 * e)) & 0x000F000Fu) | 0x64006400u;   // (1024 + q_e, 1024 + q_{e+4})
-            }
-#pragma unroll
-            for (int bb = 0; bb < B; ++bb) {
-                float dt = 0.f;
-#pragma unroll
-                for (int i = 0; i < 8; ++i) dt = dot2(np[i], xp[bb][i], dt);
-                // sum q x = dt - 1024 sx; times scale, plus offset * sx
-                acc[r][bb] = fmaf(sc, fmaf(-1024.f, sx[bb], dt), fmaf(of, sx[bb], acc[r][bb]));
-            }
-        }
+    for (int k0 = 16 * lane; k0 < K; k0 += 2048) {
+        // two steps' loads before either step's arithmetic (the second step
+        // exists for every lane or for none when K is a multiple of 1024)
+        const int k1 = k0 + 1024;
+        const bool two = k1 < K;
+        Int4W wa, wb;
+        Int4X<B> xa, xb;
+        int4_load_w<G>(wa, q, so, M, K, r0, k0);
+        if (two) int4_load_w<G>(wb, q, so, M, K, r0, k1);
+        int4_load_x<B>(xa, x, K, k0);
+        if (two) int4_load_x<B>(xb, x, K, k1);
+        int4_step<B>(acc, wa, xa);
+        if (two) int4_step<B>(acc, wb, xb);
     }
 #pragma unroll
     for (int r = 0; r < kInt4RowsPerWave; ++r)

@@ -158,6 +158,36 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t s
 
 // ================================================================== C ABI
 
+namespace {
+
+// int4 products with groups of G weights along K (K a positive multiple of G)
+template <int G>
+int int4_gemv_launch(const void* q, const uint16_t* scale_off, const uint16_t* x, float* y, int M, int K,
+                     int batch, hipStream_t stream) {
+    if (!q || !scale_off || !x || !y || M < 1 || K < G || K % G) return TETRA_EINVAL;
+    if (batch < 1 || batch > TETRA_MAX_BATCH) return TETRA_EINVAL;
+    if (!aligned(q, 8) || !aligned(scale_off, 4) || !aligned(x, 16)) return TETRA_EALIGN;
+    int dev;
+    if (int st = ensure_tables(&dev)) return st;
+    const long long waves = (static_cast<long long>(M) + tetra_dev::kInt4RowsPerWave - 1) / tetra_dev::kInt4RowsPerWave;
+    const long long grid = (waves + tetra_dev::kInt4Waves - 1) / tetra_dev::kInt4Waves;
+    if (grid > 0x7FFFFFFFLL) return TETRA_EINVAL;
+    const uint8_t* qb = static_cast<const uint8_t*>(q);
+#define TETRA_I4(B)                                                                                          \
+    case B:                                                                                                  \
+        hipLaunchKernelGGL((tetra_dev::int4_gemv_kernel<B, G>), dim3(static_cast<unsigned>(grid)),           \
+                           dim3(tetra_dev::kInt4Waves * 64), 0, stream, qb, scale_off, x, y, M, K);          \
+        break;
+    switch (batch) {
+        TETRA_I4(1) TETRA_I4(2) TETRA_I4(3) TETRA_I4(4) TETRA_I4(5) TETRA_I4(6) TETRA_I4(7) TETRA_I4(8)
+        default: return TETRA_EINVAL;
+    }
+#undef TETRA_I4
+    return launch_status();
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* tetra_status_string(int status) {
@@ -292,26 +322,12 @@ int tetra_dequant(const void* codes, const uint16_t* row_scales, int M, int K, f
 
 int tetra_int4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x, float* y, int M, int K,
                     int batch, hipStream_t stream) {
-    if (!q || !scale_off || !x || !y || M < 1 || K < tetra_dev::kInt4Group || K % tetra_dev::kInt4Group)
-        return TETRA_EINVAL;
-    if (batch < 1 || batch > TETRA_MAX_BATCH) return TETRA_EINVAL;
-    if (!aligned(q, 8) || !aligned(scale_off, 4) || !aligned(x, 16)) return TETRA_EALIGN;
-    int dev;
-    if (int st = ensure_tables(&dev)) return st;
-    const long long waves = (static_cast<long long>(M) + tetra_dev::kInt4RowsPerWave - 1) / tetra_dev::kInt4RowsPerWave;
-    const unsigned grid = static_cast<unsigned>((waves + tetra_dev::kInt4Waves - 1) / tetra_dev::kInt4Waves);
-    const uint8_t* qb = static_cast<const uint8_t*>(q);
-#define TETRA_I4(B)                                                                                        \
-    case B:                                                                                                \
-        hipLaunchKernelGGL(tetra_dev::int4_gemv_kernel<B>, dim3(grid), dim3(tetra_dev::kInt4Waves * 64), 0, \
-                           stream, qb, scale_off, x, y, M, K);                                             \
-        break;
-    switch (batch) {
-        TETRA_I4(1) TETRA_I4(2) TETRA_I4(3) TETRA_I4(4) TETRA_I4(5) TETRA_I4(6) TETRA_I4(7) TETRA_I4(8)
-        default: return TETRA_EINVAL;
-    }
-#undef TETRA_I4
-    return launch_status();
+    return int4_gemv_launch<tetra_dev::kInt4Group>(q, scale_off, x, y, M, K, batch, stream);
+}
+
+int tetra_head4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x, float* y, int rows, int dim,
+                     int batch, hipStream_t stream) {
+    return int4_gemv_launch<tetra_dev::kHead4Group>(q, scale_off, x, y, rows, dim, batch, stream);
 }
 
 int tetra_emb4_gather(const void* q, const uint16_t* scale_off, int rows, int dim, const int* tokens, int n,

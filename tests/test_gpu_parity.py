@@ -321,6 +321,64 @@ def test_int4_gemv_14b_shapes_sampled(name):
     _int4_check(M, K, 1, 800 + M + K, rows=_sample_rows(M, rng))
 
 
+# ------------------------------------------------------------------- head4
+
+def _head4_check(rows, dim, batch, seed, sample=None):
+    q, so, _ = workloads.emb4_table(seed, rows, dim)
+    x = workloads.activations(seed, batch, dim)
+    y = torch.empty((batch, rows), dtype=torch.float32, device="cuda")
+    tt.head4_gemv(_dev(q), _f16_dev(so), _f16_dev(x), y, rows, dim, batch)
+    torch.cuda.synchronize()
+    yg = y.cpu().numpy().astype(np.float64)
+    yr, norm = oint4.int4_gemv_f64(q, so, x, group=64, rows=sample)
+    if sample is not None:
+        yg = yg[:, sample]
+    worst = float((np.abs(yg - yr) / np.maximum(norm, 1e-300)).max())
+    print(f"[head4] rows={rows} dim={dim} batch={batch} worst={worst:.3e}", flush=True)
+    assert worst <= TOL
+    assert worst <= TOL_PAPER
+    return y.cpu().numpy(), x, q, so
+
+
+@pytest.mark.parametrize("rows,dim", [(1, 64), (3, 192), (130, 1024), (64, 5120), (33, 2560), (9, 1088)])
+def test_head4_gemv_small(rows, dim):
+    _head4_check(rows, dim, 1, 900 + rows)
+
+
+@pytest.mark.parametrize("batch", [1, 2, 4, 8])
+def test_head4_gemv_batches_are_invariant(batch):
+    rows, dim = 70, 5120
+    yb, x, q, so = _head4_check(rows, dim, batch, 950 + batch)
+    for b in range(batch):
+        y1 = torch.empty((1, rows), dtype=torch.float32, device="cuda")
+        tt.head4_gemv(_dev(q), _f16_dev(so), _f16_dev(x[b:b + 1]), y1, rows, dim, 1)
+        torch.cuda.synchronize()
+        assert np.array_equal(y1.cpu().numpy()[0], yb[b])
+
+
+def test_head4_gemv_full_size_sampled():
+    """The 151,936 x 5,120 head of the 14B shapes, made on the device; the
+    sampled rows are copied back for the oracle."""
+    rows, dim = 151936, 5120
+    g = torch.Generator(device="cuda").manual_seed(13)
+    qd = torch.empty((rows, dim // 2), dtype=torch.uint8, device="cuda").random_(0, 256, generator=g)
+    sod = ((torch.rand((rows, dim // 64), generator=g, device="cuda") * 1.5 + 0.5) * (1e-2 / 8))
+    sod = torch.stack([sod, -7.5 * sod], dim=-1).half().contiguous()
+    x = workloads.activations(14, 1, dim)
+    y = torch.empty((1, rows), dtype=torch.float32, device="cuda")
+    tt.head4_gemv(qd, sod, _f16_dev(x), y, rows, dim, 1)
+    torch.cuda.synchronize()
+    sample = np.array(sorted({0, 1, 63, 64, 77777, rows - 2, rows - 1}
+                             | set(np.random.default_rng(15).integers(0, rows, 57).tolist())))
+    ys = torch.as_tensor(sample, device="cuda")
+    qs, ss = qd[ys].cpu().numpy(), sod[ys].cpu().numpy()
+    yr, norm = oint4.int4_gemv_f64(qs, ss, x, group=64)
+    got = y.cpu().numpy()[:, sample].astype(np.float64)
+    worst = float((np.abs(got - yr) / np.maximum(norm, 1e-300)).max())
+    print(f"[head4] full size, {len(sample)} rows, worst={worst:.3e}", flush=True)
+    assert worst <= TOL and worst <= TOL_PAPER
+
+
 # ------------------------------------------------------------------- emb4
 
 def test_emb4_gather_bit_exact():

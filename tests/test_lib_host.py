@@ -201,7 +201,7 @@ def test_grouped_validation():
     assert lib.tetra_gemv_grouped(ctypes.cast(arr3, ctypes.c_void_p), 2, 1, None) == tt.EALIGN
 
 
-def test_int4_and_emb4_validation():
+def test_int4_head4_and_emb4_validation():
     lib = tt.library()
     fake = 0x1000
     assert lib.tetra_int4_gemv(None, fake, fake, fake, 64, 128, 1, None) == tt.EINVAL
@@ -210,6 +210,12 @@ def test_int4_and_emb4_validation():
     assert lib.tetra_int4_gemv(fake, fake, fake, fake, 64, 128, 9, None) == tt.EINVAL
     assert lib.tetra_int4_gemv(fake + 4, fake, fake, fake, 64, 128, 1, None) == tt.EALIGN
     assert lib.tetra_int4_gemv(fake, fake, fake + 8, fake, 64, 128, 1, None) == tt.EALIGN
+    assert lib.tetra_head4_gemv(None, fake, fake, fake, 64, 64, 1, None) == tt.EINVAL
+    assert lib.tetra_head4_gemv(fake, fake, fake, fake, 64, 96, 1, None) == tt.EINVAL    # dim % 64
+    assert lib.tetra_head4_gemv(fake, fake, fake, fake, 0, 64, 1, None) == tt.EINVAL
+    assert lib.tetra_head4_gemv(fake, fake, fake, fake, 64, 64, 0, None) == tt.EINVAL
+    assert lib.tetra_head4_gemv(fake, fake + 2, fake, fake, 64, 64, 1, None) == tt.EALIGN
+    assert lib.tetra_head4_gemv(fake, fake, fake + 4, fake, 64, 64, 1, None) == tt.EALIGN
     assert lib.tetra_emb4_gather(None, fake, 10, 128, fake, 1, fake, None) == tt.EINVAL
     assert lib.tetra_emb4_gather(fake, fake, 10, 96, fake, 1, fake, None) == tt.EINVAL    # dim % 64
     assert lib.tetra_emb4_gather(fake, fake, 0, 128, fake, 1, fake, None) == tt.EINVAL

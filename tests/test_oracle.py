@@ -427,3 +427,28 @@ def test_int4_affine_pins():
     diff = np.argwhere(w2 != w)
     assert diff.tolist() == [[1, 141]]
     assert np.isclose(w2[1, 141] - w[1, 141], 3 * float(so[1, 1, 0]), rtol=1e-3)
+
+
+def test_head4_groups_of_64_pins():
+    """The output head of Sec. 4.4 uses groups of 64: constant nibbles reduce
+    the product to per-group sums of x, and a one-hot x on either side of a
+    group boundary picks the weight of its own group."""
+    rng = np.random.default_rng(9)
+    rows, dim = 4, 256
+    so = rng.uniform(0.1, 1.0, (rows, dim // 64, 2)).astype(np.float16)
+    x = rng.standard_normal((1, dim)).astype(np.float16)
+    c = 11
+    q = np.full((rows, dim // 2), c | c << 4, np.uint8)
+    y, _ = int4.int4_gemv_f64(q, so, x, group=64)
+    sx = x.astype(np.float64).reshape(dim // 64, 64).sum(axis=1)          # per-group sums
+    s64 = so.astype(np.float32).astype(np.float64)
+    want = ((s64[..., 0] * c + s64[..., 1]) * sx).sum(axis=1)
+    assert np.allclose(y[0], want, rtol=1e-6)
+    q = rng.integers(0, 256, size=(rows, dim // 2), dtype=np.uint8)
+    for k in (63, 64, 127, 128):
+        e = np.zeros((1, dim), np.float16)
+        e[0, k] = 1.0
+        y, _ = int4.int4_gemv_f64(q, so, e, group=64)
+        nib = (q[:, k // 2] >> (4 * (k % 2))) & 0xF
+        want = (so[:, k // 64, 0].astype(np.float32) * nib).astype(np.float32) + so[:, k // 64, 1].astype(np.float32)
+        assert np.array_equal(y[0].astype(np.float32), want.astype(np.float32)), k
