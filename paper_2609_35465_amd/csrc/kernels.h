@@ -883,6 +883,94 @@ __global__ __launch_bounds__(kInt4Waves * 64) void int4_gemv_kernel(const uint8_
         }
 }
 
+// Large int4 launches: persistent 16-wave workgroups that stage the
+// activations once, already in the form every step uses (for each batch row
+// and 16-weight chunk: the eight permuted fp16 pairs and the chunk's sum), so
+// that the steps read them from LDS instead of fetching the vector from L2
+// for every pair of rows (that traffic was twice the weight stream).  Each
+// wave then takes row pairs rg, rg + waves, ... of the launch.
+
+constexpr int kInt4LdsWaves = 16;
+constexpr int kInt4LdsThreads = kInt4LdsWaves * 64;
+constexpr int kInt4LdsMaxBatch = 5;    // larger batches would spill at four waves per SIMD
+
+// workgroups per CU of the persistent kernel: two at batch 1 (64 VGPRs),
+// one above
+inline int int4_lds_groups_per_cu(int B) { return B == 1 ? 2 : 1; }
+
+// LDS bytes of the staged activations for K and B: [B][K/16][8] pairs, then
+// [B][K/16] sums
+__host__ __device__ constexpr size_t int4_lds_bytes(int K, int B) {
+    return static_cast<size_t>(B) * (K / 16) * (8 * 4 + 4);
+}
+
+template <int B, int G>
+__global__ __launch_bounds__(kInt4LdsThreads) __attribute__((amdgpu_waves_per_eu(B == 1 ? 8 : 4)))
+void int4_gemv_lds_kernel(const uint8_t* __restrict__ q,
+                                                                       const uint16_t* __restrict__ so,
+                                                                       const uint16_t* __restrict__ x,
+                                                                       float* __restrict__ y, int M, int K) {
+    extern __shared__ uint4 s_x4[];
+    uint32_t* s_xp = reinterpret_cast<uint32_t*>(s_x4);                 // [B][K/16][8]
+    const int chunks = K / 16;
+    float* s_sx = reinterpret_cast<float*>(s_xp + static_cast<size_t>(B) * chunks * 8);   // [B][K/16]
+    for (int c = threadIdx.x; c < chunks; c += kInt4LdsThreads) {
+        Int4X<B> a;
+        int4_load_x<B>(a, x, K, 16 * c);
+#pragma unroll
+        for (int bb = 0; bb < B; ++bb) {
+            uint4* d = reinterpret_cast<uint4*>(s_xp + (static_cast<size_t>(bb) * chunks + c) * 8);
+            d[0] = make_uint4(a.xp[bb][0], a.xp[bb][1], a.xp[bb][2], a.xp[bb][3]);
+            d[1] = make_uint4(a.xp[bb][4], a.xp[bb][5], a.xp[bb][6], a.xp[bb][7]);
+            s_sx[bb * chunks + c] = a.sx[bb];
+        }
+    }
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int pairs = (M + kInt4RowsPerWave - 1) / kInt4RowsPerWave;
+    const int waves = gridDim.x * kInt4LdsWaves;
+    for (int rg = blockIdx.x * kInt4LdsWaves + (threadIdx.x >> 6); rg < pairs; rg += waves) {
+        const int r0 = rg * kInt4RowsPerWave;
+        float acc[kInt4RowsPerWave][B];
+#pragma unroll
+        for (int r = 0; r < kInt4RowsPerWave; ++r)
+#pragma unroll
+            for (int bb = 0; bb < B; ++bb) acc[r][bb] = 0.f;
+        for (int k0 = 16 * lane; k0 < K; k0 += 2048) {
+            const int k1 = k0 + 1024;
+            const bool two = k1 < K;
+            Int4W wa, wb;
+            Int4X<B> xa;
+            int4_load_w<G>(wa, q, so, M, K, r0, k0);
+            if (two) int4_load_w<G>(wb, q, so, M, K, r0, k1);
+            auto lds_x = [&](Int4X<B>& a, int k) {
+#pragma unroll
+                for (int bb = 0; bb < B; ++bb) {
+                    const uint4* sp = reinterpret_cast<const uint4*>(s_xp + (static_cast<size_t>(bb) * chunks + k / 16) * 8);
+                    const uint4 u = sp[0], v = sp[1];
+                    a.xp[bb][0] = u.x; a.xp[bb][1] = u.y; a.xp[bb][2] = u.z; a.xp[bb][3] = u.w;
+                    a.xp[bb][4] = v.x; a.xp[bb][5] = v.y; a.xp[bb][6] = v.z; a.xp[bb][7] = v.w;
+                    a.sx[bb] = s_sx[bb * chunks + k / 16];
+                }
+            };
+            // each step's activations just before the step (one register set)
+            lds_x(xa, k0);
+            int4_step<B>(acc, wa, xa);
+            if (two) {
+                lds_x(xa, k1);
+                int4_step<B>(acc, wb, xa);
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < kInt4RowsPerWave; ++r)
+#pragma unroll
+            for (int bb = 0; bb < B; ++bb) {
+                const float v = wave_sum(acc[r][bb]);
+                if (lane == 0 && r0 + r < M) y[static_cast<size_t>(bb) * M + r0 + r] = v;
+            }
+    }
+}
+
 // ------------------------------------------------ 4-bit embedding rows
 //
 // One row of a 4-bit embedding table (Sec. 4.4): groups of 64 along the

@@ -169,12 +169,26 @@ int int4_gemv_launch(const void* q, const uint16_t* scale_off, const uint16_t* x
     if (!aligned(q, 8) || !aligned(scale_off, 4) || !aligned(x, 16)) return TETRA_EALIGN;
     int dev;
     if (int st = ensure_tables(&dev)) return st;
-    const long long waves = (static_cast<long long>(M) + tetra_dev::kInt4RowsPerWave - 1) / tetra_dev::kInt4RowsPerWave;
-    const long long grid = (waves + tetra_dev::kInt4Waves - 1) / tetra_dev::kInt4Waves;
+    const long long pairs = (static_cast<long long>(M) + tetra_dev::kInt4RowsPerWave - 1) / tetra_dev::kInt4RowsPerWave;
+    const long long grid = (pairs + tetra_dev::kInt4Waves - 1) / tetra_dev::kInt4Waves;
     if (grid > 0x7FFFFFFFLL) return TETRA_EINVAL;
     const uint8_t* qb = static_cast<const uint8_t*>(q);
+    // a launch of at least one row pair per wave of a full chip of persistent
+    // workgroups stages the activations in LDS (when they fit in 64 KB)
+    const long long lds_groups = static_cast<long long>(tetra_dev::int4_lds_groups_per_cu(batch)) * num_cus(dev);
+    const size_t lds = tetra_dev::int4_lds_bytes(K, batch);
+    const bool use_lds = batch <= tetra_dev::kInt4LdsMaxBatch &&
+                         pairs >= lds_groups * tetra_dev::kInt4LdsWaves && lds <= 65536;
 #define TETRA_I4(B)                                                                                          \
     case B:                                                                                                  \
+        if constexpr (B <= tetra_dev::kInt4LdsMaxBatch) {                                                    \
+            if (use_lds) {                                                                                   \
+                hipLaunchKernelGGL((tetra_dev::int4_gemv_lds_kernel<B, G>),                                  \
+                                   dim3(static_cast<unsigned>(lds_groups)), dim3(tetra_dev::kInt4LdsThreads), \
+                                   lds, stream, qb, scale_off, x, y, M, K);                                  \
+                break;                                                                                       \
+            }                                                                                                \
+        }                                                                                                    \
         hipLaunchKernelGGL((tetra_dev::int4_gemv_kernel<B, G>), dim3(static_cast<unsigned>(grid)),           \
                            dim3(tetra_dev::kInt4Waves * 64), 0, stream, qb, scale_off, x, y, M, K);          \
         break;

@@ -321,6 +321,37 @@ def test_int4_gemv_14b_shapes_sampled(name):
     _int4_check(M, K, 1, 800 + M + K, rows=_sample_rows(M, rng))
 
 
+def test_int4_gemv_large_launch_sampled():
+    """A launch large enough for the persistent kernel that stages the
+    activations in LDS (K = 2560: the last 1024-weight step is half-full)."""
+    M, K = 40000, 2560
+    rng = np.random.default_rng(41)
+    _int4_check(M, K, 1, 1041, rows=_sample_rows(M, rng))
+
+
+@pytest.mark.parametrize("batch", [2, 3, 5])
+def test_int4_gemv_large_batches_match_single(batch):
+    """At 12,000 rows a batch of 2-5 runs the persistent LDS kernel and batch
+    1 the per-row-pair kernel; both must give the same bits for every row
+    (K = 1152: the second step of a lane exists for 8 lanes only)."""
+    M, K = 12000, 1152
+    q, so = workloads.int4_matrix(1100 + batch, M, K)
+    x = workloads.activations(1100 + batch, batch, K)
+    qd, sd = _dev(q), _f16_dev(so)
+    yb = torch.empty((batch, M), dtype=torch.float32, device="cuda")
+    tt.int4_gemv(qd, sd, _f16_dev(x), yb, M, K, batch)
+    rows = _sample_rows(M, np.random.default_rng(batch))
+    yr, norm = oint4.int4_gemv_f64(q, so, x, rows=rows)
+    torch.cuda.synchronize()
+    got = yb.cpu().numpy()
+    assert float((np.abs(got[:, rows] - yr) / norm).max()) <= TOL_PAPER
+    for b in range(batch):
+        y1 = torch.empty((1, M), dtype=torch.float32, device="cuda")
+        tt.int4_gemv(qd, sd, _f16_dev(x[b:b + 1]), y1, M, K, 1)
+        torch.cuda.synchronize()
+        assert np.array_equal(y1.cpu().numpy()[0], got[b]), b
+
+
 # ------------------------------------------------------------------- head4
 
 def _head4_check(rows, dim, batch, seed, sample=None):
