@@ -452,3 +452,49 @@ def test_head4_groups_of_64_pins():
         nib = (q[:, k // 2] >> (4 * (k % 2))) & 0xF
         want = (so[:, k // 64, 0].astype(np.float32) * nib).astype(np.float32) + so[:, k // 64, 1].astype(np.float32)
         assert np.array_equal(y[0].astype(np.float32), want.astype(np.float32)), k
+
+
+# ----------------------------------------------------------------- rotation
+
+from oracle import rotation  # noqa: E402
+
+
+@pytest.mark.parametrize("n", [1, 2, 4, 8, 16, 64])
+def test_hadamard_is_sylvester_and_orthogonal(n):
+    """H_n: entries +-1, H H^T = n I, and the Sylvester recursion."""
+    from scipy.linalg import hadamard
+    h = hadamard(n)
+    assert set(np.unique(h).tolist()) <= {-1, 1}
+    assert np.array_equal(h @ h.T, n * np.eye(n, dtype=h.dtype))
+    if n > 1:
+        q = hadamard(n // 2)
+        assert np.array_equal(h, np.block([[q, q], [q, -q]]))
+    # entry (i, m) is (-1)^popcount(i & m) (the Walsh-Hadamard form)
+    for i in range(n):
+        for m in range(n):
+            assert h[i, m] == (-1) ** bin(i & m).count("1")
+
+
+def test_rotation_pins():
+    """Norm preservation per block, involution of the unsigned transform,
+    the sign convention, and a one-hot column."""
+    rng = np.random.default_rng(21)
+    n, K = 64, 256
+    x = rng.standard_normal((2, K)).astype(np.float16)
+    bits = rng.integers(0, 256, K // 8, dtype=np.uint8)
+    y = rotation.rotate_f64(x, bits, n)
+    xb = x.astype(np.float64).reshape(2, K // n, n)
+    assert np.allclose(np.linalg.norm(y.reshape(2, K // n, n), axis=-1), np.linalg.norm(xb, axis=-1), rtol=1e-12)
+    zero = np.zeros(K // 8, np.uint8)
+    twice = rotation.rotate_f64(rotation.rotate_f64(x, zero, n).astype(np.float64), zero, n)
+    assert np.allclose(twice, x.astype(np.float64), atol=1e-3)      # the inner result was rounded to fp16
+    # sign bit k negates element k before the transform
+    one = np.zeros((1, K), np.float16)
+    one[0, 5] = 1.0
+    b5 = np.zeros(K // 8, np.uint8)
+    b5[0] = 1 << 5
+    assert np.allclose(rotation.rotate_f64(one, b5, n), -rotation.rotate_f64(one, zero, n))
+    full = rotation.rotate_f64(one, zero, n)[0]
+    want = np.array([(-1) ** bin(i & 5).count("1") for i in range(n)]) / np.sqrt(n)
+    assert np.allclose(full[:n], want, rtol=1e-15)
+    assert not full[n:].any()                                       # blocks do not mix
