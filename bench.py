@@ -52,11 +52,12 @@ def parse():
                     help="matrix: one launch per matrix; deps: per layer [q,k,v] [o] "
                          "[gate,up] [down] (the launches a decode step can fuse); "
                          "layer: one grouped launch per layer")
-    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4", "head"],
+    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4", "head", "rotate"],
                     help="tetra: every projection a Tetra matrix (the GEMV metric); c4: the "
                          "full decode step -- 10%% of the projections (seeded) stored as int4 "
                          "w4g128 and one 4-bit embedding row gathered per step; head: the "
-                         "4-bit output head GEMV (151936 x 5120, groups of 64) alone")
+                         "4-bit output head GEMV (151936 x 5120, groups of 64) alone; rotate: "
+                         "the online activation rotations of one layer")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the benchmark: copy a buffer of this many MiB five "
                          "times with torch (a plain copy kernel of known size, the "
@@ -392,6 +393,83 @@ def main_head(args, torch, tt):
     return 0
 
 
+def main_rotate(args, torch, tt):
+    """The online activation rotation at the 14B widths: per decode layer one
+    rotation of the hidden vector (5,120, blocks of 1,024) for the q/k/v and
+    gate/up groups each, one of the attention output (5,120) for o, and one of
+    the intermediate vector (17,408, blocks of 1,024) for down.  A step is the
+    four rotations of one layer, replayed from a HIP graph."""
+    from oracle import rotation as orot
+    from paper_2609_35465_amd import workloads
+    B = args.batch
+    widths = [(5120, 1024), (5120, 1024), (5120, 1024), (17408, 1024)]
+    rng = np.random.default_rng(0x7E7A_0060)
+    bufs = []
+    for K, n in widths:
+        x = torch.as_tensor(workloads.activations(0x7E7A_0060 + K, B, K)).cuda()
+        bits = torch.as_tensor(rng.integers(0, 256, (K + 7) // 8, dtype=np.uint8)).cuda()
+        bufs.append((x, bits, torch.empty_like(x), K, n))
+    stream = torch.cuda.current_stream()
+
+    def step(s=None):
+        st = (s or stream).cuda_stream
+        for x, bits, out, K, n in bufs:
+            tt.rotate(x, bits, out, K, n, B, stream=st)
+
+    step()
+    torch.cuda.synchronize()
+    worst = 0.0
+    for x, bits, out, K, n in bufs:
+        ref = orot.rotate_f64(x.cpu().numpy(), bits.cpu().numpy(), n)
+        got = out.cpu().numpy().astype(np.float64)
+        worst = max(worst, float((np.abs(got - ref) / np.maximum(np.abs(ref), 1e-3)).max()))
+    graph = None
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(torch.cuda.current_stream())
+    run = graph.replay if graph is not None else step
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    algo = sum(4 * K * B + (K + 7) // 8 for _, _, _, K, _ in bufs)
+    value = algo / (ms_step * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32 (fp16 in/out)", "data": "synthetic",
+        "config": {"workload": f"online rotation of one 14B layer's activations: 3 x 5120 + 17408, "
+                               f"Hadamard blocks of 1024, batch {B}", "batch": B, "hip_graph": graph is not None},
+        "us_per_rotation": round(ms_step * 1e3 / len(bufs), 3),
+        "rotate_worst_rel_err": worst,
+        "roofline": {"bound": "hbm", "achieved": round(value, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(value / HBM_PEAK_GBS, 6), "traffic": None, "kernel": "rotate_kernel",
+                     "avg_launch_us": round(ms_step * 1e3 / len(bufs), 3),
+                     "bytes_per_launch": round(algo / len(bufs))},
+    }
+    if not args.no_cpu_baseline:
+        xs = [(x.cpu().numpy(), bits.cpu().numpy(), K, n) for x, bits, _, K, n in bufs]
+        t_used, done = 0.0, 0
+        while t_used < min(args.cpu_seconds, 10.0):
+            for xh, bh, K, n in xs:
+                t0 = time.perf_counter()
+                orot.rotate_f64(xh, bh, n)
+                t_used += time.perf_counter() - t0
+            done += 1
+        out["cpu_baseline"] = {"value": round(done * algo / t_used / 1e9, 6), "unit": "GB/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{done} layers' rotations (dense float64 Hadamard blocks) in {t_used:.1f} s"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -416,6 +494,8 @@ def main():
         return 0
     if args.workload == "head":
         return main_head(args, torch, tt)
+    if args.workload == "rotate":
+        return main_rotate(args, torch, tt)
     stream = torch.cuda.current_stream()
     plan, L, emb = build_workload(torch, tt, args.model, args.layers, args.batch, args.workload)
     torch.cuda.synchronize()

@@ -227,6 +227,26 @@ int tetra_head4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x
                      int batch, hipStream_t stream);
 
 /*
+ * Online rotation of the activations (Sec. 3.1, Sec. 5.1): the randomized
+ * Hadamard transform that the encoder applied to the weights, applied to x
+ * before the products that share it.  The paper names no construction; the
+ * reading taken is blockwise: for each block of n consecutive elements of a
+ * row (j0 a multiple of n),
+ *   out[b][j0 + i] = fp16( (1/sqrt n) * sum_m H_n[i][m] * s[j0+m] * x[b][j0+m] )
+ * with H_n the Sylvester Hadamard matrix (H_n[i][m] = (-1)^popcount(i & m))
+ * and s[k] = -1 where bit k % 8 of sign_bits[k / 8] is set, else +1.  The
+ * signs are the caller's (drawn once per group of projections).  Computed in
+ * fp32, rounded to nearest even at the end.
+ *   x:         device fp16 [rows][K], 8-byte aligned
+ *   sign_bits: device bytes [ceil(K / 8)]
+ *   out:       device fp16 [rows][K], 8-byte aligned; may be x itself
+ * n must be a power of two in [4, 4096] dividing K; rows 1..65535.
+ * Asynchronous; TETRA_EINVAL / TETRA_EALIGN / TETRA_EDEVICE as for tetra_gemv.
+ */
+int tetra_rotate(const uint16_t* x, const uint8_t* sign_bits, uint16_t* out, int K, int n, int rows,
+                 hipStream_t stream);
+
+/*
  * Rows of a 4-bit embedding table (Sec. 4.4): groups of 64 along the
  * embedding dimension, fp16 scale and offset per group, nibbles as in
  * tetra_int4_gemv;  out[i][k] = fl32(fl32(scale * q) + offset) for the row

@@ -37,6 +37,7 @@ _SIGNATURES = {
     "tetra_dequant": (_int, [_vp, _vp, _int, _int, _vp, _vp]),
     "tetra_int4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_head4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
+    "tetra_rotate": (_int, [_vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_emb4_gather": (_int, [_vp, _vp, _int, _int, _vp, _int, _vp, _vp]),
 }
 EXPORTED = tuple(_SIGNATURES)
@@ -183,6 +184,13 @@ def head4_gemv(q, scale_off, x, y, rows: int, dim: int, batch: int = 1, stream=N
     scale_off fp16 [rows, dim/64, 2], x fp16 [batch, dim] (device tensors)."""
     _check(_call("tetra_head4_gemv", _ptr(q), _ptr(scale_off), _ptr(x), _ptr(y), rows, dim, batch,
                  _stream(stream)), "tetra_head4_gemv")
+
+
+def rotate(x, sign_bits, out, K: int, n: int, rows: int = 1, stream=None):
+    """out[rows, K] fp16 = blockwise randomized Hadamard transform of x
+    (blocks of n) with the signs in sign_bits (uint8 [ceil(K/8)]); out may be x."""
+    _check(_call("tetra_rotate", _ptr(x), _ptr(sign_bits), _ptr(out), K, n, rows, _stream(stream)),
+           "tetra_rotate")
 
 
 def emb4_gather(q, scale_off, rows: int, dim: int, tokens, out, stream=None):

@@ -23,6 +23,11 @@ __device__ __forceinline__ float f16(uint16_t v) {
     return static_cast<float>(__builtin_bit_cast(_Float16, v));
 }
 
+// fp16 bits of a float, round to nearest even
+__device__ __forceinline__ uint16_t f16_bits(float v) {
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(v));
+}
+
 // the lane index, computed afresh at each use: the cold paths of the GEMV
 // (tile tails, single columns, piece reduction) take their lane addresses
 // from it, so that none of them is hoisted and kept live across the hot loop
@@ -968,6 +973,81 @@ void int4_gemv_lds_kernel(const uint8_t* __restrict__ q,
                 const float v = wave_sum(acc[r][bb]);
                 if (lane == 0 && r0 + r < M) y[static_cast<size_t>(bb) * M + r0 + r] = v;
             }
+    }
+}
+
+// ------------------------------------------------- activation rotation
+//
+// The online rotation of the activations (Sec. 3.1, Sec. 5.1): a randomized
+// Hadamard transform, block by block.  For each block of n = 2^k elements,
+//   out[j0 + i] = (1/sqrt n) sum_m H_n[i][m] s[j0 + m] x[j0 + m],
+// H_n the Sylvester Hadamard matrix, s = -1 where the caller's sign bit is
+// set.  A workgroup of T threads takes a segment of 4T elements of one
+// batch row (T = 256 for n <= 1024, so a segment holds whole blocks; T = n/4
+// above), four consecutive elements per thread.  The butterflies of strides
+// 1 and 2 stay in the thread, strides up to 128 go through lane shuffles,
+// larger ones through LDS.  fp32 throughout, rounded to fp16 at the end.
+
+template <int T>
+__global__ __launch_bounds__(T) void rotate_kernel(const uint16_t* __restrict__ x, const uint8_t* __restrict__ bits,
+                                                   uint16_t* out, int K, int n, float scale) {
+    __shared__ float s_v[4 * T];
+    const int t = threadIdx.x;
+    const long long row = blockIdx.y;
+    const int k = blockIdx.x * (4 * T) + 4 * t;     // first element of this thread
+    const bool live = k < K;                        // K is a multiple of 4 and of n
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (live) {
+        const uint2 u = *reinterpret_cast<const uint2*>(x + row * K + k);
+        const uint32_t sb = bits[k >> 3] >> (k & 7);   // k is a multiple of 4: four bits in one byte
+        v[0] = f16(static_cast<uint16_t>(u.x));
+        v[1] = f16(static_cast<uint16_t>(u.x >> 16));
+        v[2] = f16(static_cast<uint16_t>(u.y));
+        v[3] = f16(static_cast<uint16_t>(u.y >> 16));
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (sb >> e & 1u) v[e] = -v[e];
+    }
+    // strides 1 and 2: inside the thread
+    {
+        const float a0 = v[0] + v[1], a1 = v[0] - v[1], a2 = v[2] + v[3], a3 = v[2] - v[3];
+        v[0] = a0;
+        v[1] = a1;
+        v[2] = a2;
+        v[3] = a3;
+        if (n > 2) {
+            const float b0 = v[0] + v[2], b1 = v[1] + v[3], b2 = v[0] - v[2], b3 = v[1] - v[3];
+            v[0] = b0;
+            v[1] = b1;
+            v[2] = b2;
+            v[3] = b3;
+        }
+    }
+    // strides 4 .. n/2: partner thread t ^ (h / 4); the thread whose bit is
+    // set keeps the difference partner - own, the other the sum
+    for (int h = 4; h < n; h <<= 1) {
+        const int d = h >> 2;
+        const bool hi = (t & d) != 0;
+        float p[4];
+        if (d < 64) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) p[e] = __shfl_xor(v[e], d, 64);
+        } else {
+            __syncthreads();                         // the previous exchange has been read
+#pragma unroll
+            for (int e = 0; e < 4; ++e) s_v[4 * t + e] = v[e];
+            __syncthreads();
+#pragma unroll
+            for (int e = 0; e < 4; ++e) p[e] = s_v[4 * (t ^ d) + e];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = hi ? p[e] - v[e] : v[e] + p[e];
+    }
+    if (live) {
+        uint2 o;
+        o.x = static_cast<uint32_t>(f16_bits(v[0] * scale)) | static_cast<uint32_t>(f16_bits(v[1] * scale)) << 16;
+        o.y = static_cast<uint32_t>(f16_bits(v[2] * scale)) | static_cast<uint32_t>(f16_bits(v[3] * scale)) << 16;
+        *reinterpret_cast<uint2*>(out + row * K + k) = o;
     }
 }
 

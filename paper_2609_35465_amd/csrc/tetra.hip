@@ -3,6 +3,8 @@
 // tables once per device and launches the kernels of kernels.h.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+
 #include <algorithm>
 #include <cstring>
 #include <mutex>
@@ -342,6 +344,31 @@ int tetra_int4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x,
 int tetra_head4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x, float* y, int rows, int dim,
                      int batch, hipStream_t stream) {
     return int4_gemv_launch<tetra_dev::kHead4Group>(q, scale_off, x, y, rows, dim, batch, stream);
+}
+
+int tetra_rotate(const uint16_t* x, const uint8_t* sign_bits, uint16_t* out, int K, int n, int rows,
+                 hipStream_t stream) {
+    if (!x || !sign_bits || !out || n < 4 || n > 4096 || (n & (n - 1)) || K < n || K % n) return TETRA_EINVAL;
+    if (rows < 1 || rows > 65535) return TETRA_EINVAL;
+    if (!aligned(x, 8) || !aligned(out, 8)) return TETRA_EALIGN;
+    int dev;
+    if (int st = ensure_tables(&dev)) return st;
+    const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(n)));
+    const int T = n <= 1024 ? 256 : n / 4;
+    const dim3 grid(static_cast<unsigned>((K + 4 * T - 1) / (4 * T)), static_cast<unsigned>(rows));
+    switch (T) {
+        case 256:
+            hipLaunchKernelGGL(tetra_dev::rotate_kernel<256>, grid, dim3(256), 0, stream, x, sign_bits, out, K, n, scale);
+            break;
+        case 512:
+            hipLaunchKernelGGL(tetra_dev::rotate_kernel<512>, grid, dim3(512), 0, stream, x, sign_bits, out, K, n, scale);
+            break;
+        default:
+            hipLaunchKernelGGL(tetra_dev::rotate_kernel<1024>, grid, dim3(1024), 0, stream, x, sign_bits, out, K, n,
+                               scale);
+            break;
+    }
+    return launch_status();
 }
 
 int tetra_emb4_gather(const void* q, const uint16_t* scale_off, int rows, int dim, const int* tokens, int n,

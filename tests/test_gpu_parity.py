@@ -454,3 +454,61 @@ def test_emb4_gather_full_size_table():
         sr = sod[int(t)].cpu().numpy()[None]
         want = oint4.emb4_row(qr, sr, 0)
         assert np.array_equal(got[i].view(np.uint32), want.view(np.uint32)), t
+
+
+# --------------------------------------------------------------- rotation
+
+from oracle import rotation as orot  # noqa: E402
+
+
+def _rotate_check(K, n, rows, seed, inplace=False):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((rows, K)).astype(np.float16)
+    bits = rng.integers(0, 256, (K + 7) // 8, dtype=np.uint8)
+    xd = _f16_dev(x)
+    out = xd if inplace else torch.empty_like(xd)
+    tt.rotate(xd, _dev(bits), out, K, n, rows)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.float16).astype(np.float64)
+    ref = orot.rotate_f64(x, bits, n)
+    # bound: one fp16 ulp of the result, or the fp32 accumulation error of
+    # log2(n) rounded additions over the block, whichever is larger
+    absx = np.abs(x.astype(np.float64)).reshape(rows, K // n, n).sum(axis=-1, keepdims=True)
+    acc = np.broadcast_to(absx * np.log2(n) * 2.0 ** -23 / np.sqrt(n), (rows, K // n, n)).reshape(rows, K)
+    tol = np.maximum(np.spacing(np.abs(ref).astype(np.float16)).astype(np.float64), acc)
+    bad = np.abs(got - ref) > tol
+    print(f"[rotate] K={K} n={n} rows={rows} worst/tol={float((np.abs(got - ref) / tol).max()):.3f}", flush=True)
+    assert not bad.any()
+    return got
+
+
+@pytest.mark.parametrize("n", [4, 8, 64, 128, 256, 512, 1024, 2048, 4096])
+def test_rotate_matches_oracle(n):
+    for m, rows in ((1, 1), (3, 2), (5, 1)):
+        _rotate_check(n * m, n, rows, 31 * n + m)
+
+
+@pytest.mark.parametrize("K,n", [(5120, 1024), (2560, 512), (17408, 1024), (1152, 128)])
+def test_rotate_projection_widths_and_in_place(K, n):
+    a = _rotate_check(K, n, 3, 7 + K)
+    b = _rotate_check(K, n, 3, 7 + K, inplace=True)
+    assert np.array_equal(a, b)
+
+
+def test_rotate_one_hot_is_exact():
+    """x = e_k gives column k of H_n / sqrt(n); for n = 4^j those are +-2^-j,
+    exact in fp16."""
+    for n in (4, 16, 256, 4096):
+        K = 2 * n
+        for k in (0, 1, n - 1, n + min(5, n - 1)):
+            x = np.zeros((1, K), np.float16)
+            x[0, k] = 1.0
+            bits = np.zeros((K + 7) // 8, np.uint8)
+            out = torch.empty((1, K), dtype=torch.float16, device="cuda")
+            tt.rotate(_f16_dev(x), _dev(bits), out, K, n, 1)
+            torch.cuda.synchronize()
+            got = out.cpu().numpy()[0].astype(np.float64)
+            j0 = (k // n) * n
+            want = np.zeros(K)
+            want[j0:j0 + n] = [(-1) ** bin(i & (k - j0)).count("1") / np.sqrt(n) for i in range(n)]
+            assert np.array_equal(got, want), (n, k)

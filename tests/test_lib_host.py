@@ -216,6 +216,14 @@ def test_int4_head4_and_emb4_validation():
     assert lib.tetra_head4_gemv(fake, fake, fake, fake, 64, 64, 0, None) == tt.EINVAL
     assert lib.tetra_head4_gemv(fake, fake + 2, fake, fake, 64, 64, 1, None) == tt.EALIGN
     assert lib.tetra_head4_gemv(fake, fake, fake + 4, fake, 64, 64, 1, None) == tt.EALIGN
+    assert lib.tetra_rotate(None, fake, fake, 1024, 256, 1, None) == tt.EINVAL
+    assert lib.tetra_rotate(fake, fake, fake, 1024, 96, 1, None) == tt.EINVAL       # n not a power of two
+    assert lib.tetra_rotate(fake, fake, fake, 1024, 2, 1, None) == tt.EINVAL        # n < 4
+    assert lib.tetra_rotate(fake, fake, fake, 8192, 8192, 1, None) == tt.EINVAL     # n > 4096
+    assert lib.tetra_rotate(fake, fake, fake, 1000, 256, 1, None) == tt.EINVAL      # n does not divide K
+    assert lib.tetra_rotate(fake, fake, fake, 1024, 256, 0, None) == tt.EINVAL
+    assert lib.tetra_rotate(fake + 4, fake, fake, 1024, 256, 1, None) == tt.EALIGN
+    assert lib.tetra_rotate(fake, fake, fake + 2, 1024, 256, 1, None) == tt.EALIGN
     assert lib.tetra_emb4_gather(None, fake, 10, 128, fake, 1, fake, None) == tt.EINVAL
     assert lib.tetra_emb4_gather(fake, fake, 10, 96, fake, 1, fake, None) == tt.EINVAL    # dim % 64
     assert lib.tetra_emb4_gather(fake, fake, 0, 128, fake, 1, fake, None) == tt.EINVAL
