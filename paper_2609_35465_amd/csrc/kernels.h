@@ -438,29 +438,32 @@ __device__ __forceinline__ ItemWords load_group(const uint8_t* tb, int j, int la
 }
 
 // code words of the rem = nblk mod 4 trailing columns of a tile (rem > 0),
-// whole loads straight into the item registers; the words of columns past
-// rem are left unset and never read
+// with the same five 4-byte loads whatever rem is (no branch, so that the
+// loads never wait for one another): the 32-bit parts of columns
+// min(k, rem - 1), and the 4-byte words that hold the 16-bit parts.  Where a
+// 16-bit part shares its word with the neighbouring row's (rem = 1, and the
+// third column of rem = 3), hi_shift tells how far to shift it down; the
+// shift is applied when the words are used (trailing_fixup).
 __device__ __forceinline__ ItemWords load_trailing(const uint8_t* tb, int ng, int rem) {
     const uint8_t* sp = tb + static_cast<size_t>(ng) * tetra::kGroupBytes;
     const int lane = lane_now();
+    const uint32_t* lo = reinterpret_cast<const uint32_t*>(sp + 4 * rem * lane);
+    const int h01 = rem == 1 ? 256 + 4 * (lane >> 1) : 256 * rem + 4 * lane;
+    const int h2 = rem == 3 ? 1024 + 4 * (lane >> 1) : h01;
     ItemWords w;
-    if (rem == 1) {
-        w.lo.x = *reinterpret_cast<const uint32_t*>(sp + 4 * lane);
-        w.hi.x = *reinterpret_cast<const uint16_t*>(sp + 256 + 2 * lane);
-    } else if (rem == 2) {
-        const u32x2 l = *reinterpret_cast<const u32x2*>(sp + 8 * lane);
-        w.lo.x = l.x;
-        w.lo.y = l.y;
-        w.hi.x = *reinterpret_cast<const uint32_t*>(sp + 512 + 4 * lane);
-    } else {
-        const u32x3 l = *reinterpret_cast<const u32x3*>(sp + 12 * lane);
-        w.lo.x = l.x;
-        w.lo.y = l.y;
-        w.lo.z = l.z;
-        w.hi.x = *reinterpret_cast<const uint32_t*>(sp + 768 + 4 * lane);
-        w.hi.y = *reinterpret_cast<const uint16_t*>(sp + 1024 + 2 * lane);
-    }
+    w.lo.x = lo[0];
+    w.lo.y = lo[min(1, rem - 1)];
+    w.lo.z = lo[min(2, rem - 1)];
+    w.hi.x = *reinterpret_cast<const uint32_t*>(sp + h01);
+    w.hi.y = *reinterpret_cast<const uint32_t*>(sp + h2);
     return w;
+}
+
+// the 16-bit parts of the trailing columns in place (see load_trailing)
+__device__ __forceinline__ void trailing_fixup(ItemWords& w, int rem) {
+    const uint32_t odd = (lane_now() & 1) ? 16u : 0u;
+    if (rem == 1) w.hi.x >>= odd;
+    w.hi.y >>= odd;            // only used when rem = 3
 }
 
 // A piece of a tile: block columns c0..c1-1 of tile t, in groups j..jg and,
@@ -559,8 +562,10 @@ __device__ __forceinline__ void run_piece(const GemvProblem& P, Piece& pc, lds_b
     }
     if (pc.tr) {
         const int c = 4 * P.ng;
-        start_pipe<B>(st, pc.tw, kb, c + kb, L, xc, kp);
-        run_item<B, false>(st, pc.tw, pc.tw, c, c, kb, pc.c1 - c, L, xc, kp);
+        ItemWords tw = pc.tw;
+        trailing_fixup(tw, P.rem);
+        start_pipe<B>(st, tw, kb, c + kb, L, xc, kp);
+        run_item<B, false>(st, tw, tw, c, c, kb, pc.c1 - c, L, xc, kp);
         __builtin_amdgcn_s_waitcnt(0xC07F);
         finish_pending<B>(st);
     }
