@@ -185,6 +185,22 @@ int tetra_decode(const void* words, size_t n, int8_t* y_out, float* blk_scale_ou
                  hipStream_t stream);
 
 /*
+ * The same product for many activation rows (a prompt run in one call,
+ * Sec. 6): y[n][row] for n < N, formed as in tetra_gemv (exact decoded
+ * values, each block's products scaled by its block scale in fp32, sigma and
+ * the unquantised tail at the end), with the products on the matrix cores.
+ *   codes / row_scales as in tetra_gemv (16-byte aligned codes)
+ *   x: device fp16 [N][K], 16-byte aligned; K must be a multiple of 8
+ *   y: device fp32 [N][M], fully overwritten
+ * N >= 1 (up to 65535 * 128).  Meant for N well above TETRA_MAX_BATCH; the
+ * rounding differs from tetra_gemv's (another summation order), within the
+ * same bound.  Asynchronous; TETRA_EINVAL / TETRA_EALIGN / TETRA_EDEVICE as
+ * for tetra_gemv.
+ */
+int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
+               hipStream_t stream);
+
+/*
  * Dense reconstruction of a packed matrix (Eq. 2), for testing:
  *   w_out[row][24*blk+j] = fl32(fl32(y_j * s_blk) * sigma_row),
  *   w_out[row][24*nblk+t] = tail[row][t].

@@ -38,6 +38,7 @@ _SIGNATURES = {
     "tetra_int4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_head4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_rotate": (_int, [_vp, _vp, _vp, _int, _int, _int, _vp]),
+    "tetra_gemm": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_emb4_gather": (_int, [_vp, _vp, _int, _int, _vp, _int, _vp, _vp]),
 }
 EXPORTED = tuple(_SIGNATURES)
@@ -138,6 +139,12 @@ def gemv(codes, row_scales, x, y, M: int, K: int, batch: int = 1, stream=None):
     """y[batch, M] = W x for a packed Tetra matrix (all device tensors)."""
     _check(_call("tetra_gemv", _ptr(codes), _ptr(row_scales), _ptr(x), _ptr(y), M, K, batch,
                      _stream(stream)), "tetra_gemv")
+
+
+def gemm(codes, row_scales, x, y, M: int, K: int, N: int, stream=None):
+    """y[N, M] = W x for N activation rows (a prompt), on the matrix cores."""
+    _check(_call("tetra_gemm", _ptr(codes), _ptr(row_scales), _ptr(x), _ptr(y), M, K, N, _stream(stream)),
+           "tetra_gemm")
 
 
 class Problem(ctypes.Structure):

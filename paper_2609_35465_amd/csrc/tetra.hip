@@ -13,6 +13,7 @@
 #include "../../include/tetra.h"
 #include "device_tables.h"
 #include "kernels.h"
+#include "prefill.h"
 #include "tables.h"
 #include "word_format.h"
 
@@ -344,6 +345,34 @@ int tetra_int4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x,
 int tetra_head4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x, float* y, int rows, int dim,
                      int batch, hipStream_t stream) {
     return int4_gemv_launch<tetra_dev::kHead4Group>(q, scale_off, x, y, rows, dim, batch, stream);
+}
+
+int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
+               hipStream_t stream) {
+    if (!codes || !row_scales || !x || !y || M < 1 || K < 24 || N < 1 || K % 8) return TETRA_EINVAL;
+    if (!aligned(codes, 16) || !aligned(x, 16) || !aligned(row_scales, 2) || !aligned(y, 4)) return TETRA_EALIGN;
+    const long long token_groups = (static_cast<long long>(N) + tetra_dev::kPfTokens - 1) / tetra_dev::kPfTokens;
+    if (token_groups > 65535) return TETRA_EINVAL;
+    int dev;
+    if (int st = ensure_tables(&dev)) return st;
+    Shape s;
+    if (!shape_of(M, K, &s)) return TETRA_EINVAL;
+    tetra_dev::GemmArgs a;
+    a.codes = static_cast<const uint8_t*>(codes);
+    a.sigma = row_scales;
+    a.x = x;
+    a.y = y;
+    a.tail_off = s.tail_off;
+    a.M = M;
+    a.K = K;
+    a.N = N;
+    a.nblk = s.nblk;
+    a.T = s.T;
+    a.ng = s.nblk / tetra::kGroupCols;
+    a.rem = s.nblk % tetra::kGroupCols;
+    hipLaunchKernelGGL(tetra_dev::gemm_kernel, dim3(static_cast<unsigned>(s.tiles), static_cast<unsigned>(token_groups)),
+                       dim3(tetra_dev::kPfThreads), 0, stream, a);
+    return launch_status();
 }
 
 int tetra_rotate(const uint16_t* x, const uint8_t* sign_bits, uint16_t* out, int K, int n, int rows,

@@ -512,3 +512,50 @@ def test_rotate_one_hot_is_exact():
             want = np.zeros(K)
             want[j0:j0 + n] = [(-1) ** bin(i & (k - j0)).count("1") / np.sqrt(n) for i in range(n)]
             assert np.array_equal(got, want), (n, k)
+
+
+# ----------------------------------------------------------------- prefill
+
+def _check_gemm(pk, x, rows=None, label=""):
+    N = x.shape[0]
+    y = torch.empty((N, pk.M), dtype=torch.float32, device="cuda")
+    tt.gemm(pk.blob, pk.sigma, _f16_dev(x), y, pk.M, pk.K, N)
+    torch.cuda.synchronize()
+    yg = y.cpu().numpy()
+    yr, norm = ogemv.gemv_f64(pk.words, pk.sigma_h, pk.tail, x, rows=rows)
+    if rows is not None:
+        yg = yg[:, rows]
+    worst = float((np.abs(yg.astype(np.float64) - yr) / np.maximum(norm, 1e-300)).max())
+    print(f"[gemm {label}] M={pk.M} K={pk.K} N={N} worst={worst:.3e}", flush=True)
+    assert worst <= TOL
+    assert worst <= TOL_PAPER
+    return yg
+
+
+@pytest.mark.parametrize("M,K", [(1, 24), (64, 48), (63, 80), (65, 232), (127, 120), (130, 272), (200, 1536),
+                                 (1536, 1536)])
+@pytest.mark.parametrize("N", [1, 33, 203])
+def test_gemm_small_shapes(M, K, N):
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(0, 5) + M + K, M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(M + K + N, N, K)
+    _check_gemm(pk, x, label="small")
+
+
+@pytest.mark.parametrize("N", [128, 129, 300])
+def test_gemm_token_tiles(N):
+    """Token counts on, just past and well past the 128-token workgroup."""
+    M, K = 70, 24 * 9 + 16
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(0, 6) + N, M, K)
+    pk = Packed(words, sigma, tail, K)
+    _check_gemm(pk, workloads.activations(N, N, K), label="tokens")
+
+
+@pytest.mark.parametrize("name", ["q", "gate", "down"])
+def test_gemm_14b_shapes_sampled(name):
+    shapes = {n: (M, K) for n, M, K in workloads.layer_shapes("14B")}
+    M, K = shapes[name]
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(3, len(name)), M, K)
+    pk = Packed(words, sigma, tail, K)
+    rng = np.random.default_rng(77 + len(name))
+    _check_gemm(pk, workloads.activations(len(name), 203, K), rows=_sample_rows(M, rng, n=96), label=name)

@@ -216,6 +216,12 @@ def test_int4_head4_and_emb4_validation():
     assert lib.tetra_head4_gemv(fake, fake, fake, fake, 64, 64, 0, None) == tt.EINVAL
     assert lib.tetra_head4_gemv(fake, fake + 2, fake, fake, 64, 64, 1, None) == tt.EALIGN
     assert lib.tetra_head4_gemv(fake, fake, fake + 4, fake, 64, 64, 1, None) == tt.EALIGN
+    assert lib.tetra_gemm(None, fake, fake, fake, 64, 96, 16, None) == tt.EINVAL
+    assert lib.tetra_gemm(fake, fake, fake, fake, 64, 100, 16, None) == tt.EINVAL   # K % 8
+    assert lib.tetra_gemm(fake, fake, fake, fake, 64, 96, 0, None) == tt.EINVAL
+    assert lib.tetra_gemm(fake, fake, fake, fake, 0, 96, 16, None) == tt.EINVAL
+    assert lib.tetra_gemm(fake + 8, fake, fake, fake, 64, 96, 16, None) == tt.EALIGN
+    assert lib.tetra_gemm(fake, fake, fake + 8, fake, 64, 96, 16, None) == tt.EALIGN
     assert lib.tetra_rotate(None, fake, fake, 1024, 256, 1, None) == tt.EINVAL
     assert lib.tetra_rotate(fake, fake, fake, 1024, 96, 1, None) == tt.EINVAL       # n not a power of two
     assert lib.tetra_rotate(fake, fake, fake, 1024, 2, 1, None) == tt.EINVAL        # n < 4
