@@ -52,12 +52,13 @@ def parse():
                     help="matrix: one launch per matrix; deps: per layer [q,k,v] [o] "
                          "[gate,up] [down] (the launches a decode step can fuse); "
                          "layer: one grouped launch per layer")
-    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4", "head", "rotate"],
+    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4", "head", "rotate", "prefill"],
                     help="tetra: every projection a Tetra matrix (the GEMV metric); c4: the "
                          "full decode step -- 10%% of the projections (seeded) stored as int4 "
                          "w4g128 and one 4-bit embedding row gathered per step; head: the "
                          "4-bit output head GEMV (151936 x 5120, groups of 64) alone; rotate: "
-                         "the online activation rotations of one layer")
+                         "the online activation rotations of one layer; prefill: a 203-token "
+                         "prompt through the Tetra projections on the matrix cores")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the benchmark: copy a buffer of this many MiB five "
                          "times with torch (a plain copy kernel of known size, the "
@@ -470,6 +471,104 @@ def main_rotate(args, torch, tt):
     return 0
 
 
+PREFILL_TOKENS = 203
+MFMA_F16_PEAK_TFLOPS = 2500.0
+
+
+def main_prefill(args, torch, tt):
+    """A prompt through the Tetra projections: the 14B linear set of
+    `--layers` layers (default 4) at 203 tokens, one tetra_gemm launch per
+    matrix, replayed from a HIP graph."""
+    from paper_2609_35465_amd import workloads
+    from oracle import gemv as ogemv
+    N = PREFILL_TOKENS
+    L = args.layers or 4
+    shapes = workloads.layer_shapes(args.model)
+    gen = torch.Generator(device="cuda").manual_seed(0x7E7A_0070)
+    mats, xs = [], {}
+    for layer in range(L):
+        for i, (name, M, K) in enumerate(shapes):
+            m = Matrix(torch, tt, name, M, K, gen, workloads.seed_for(3, layer * len(shapes) + i))
+            if K not in xs:
+                xs[K] = torch.as_tensor(workloads.activations(0x7E7A_0070 + K, N, K)).cuda()
+            mats.append((m, xs[K], torch.empty((N, M), dtype=torch.float32, device="cuda")))
+    stream = torch.cuda.current_stream()
+
+    def step(s=None):
+        st = (s or stream).cuda_stream
+        for m, x, y in mats:
+            tt.gemm(m.blob, m.sigma, x, y, m.M, m.K, N, stream=st)
+
+    step()
+    torch.cuda.synchronize()
+    # parity: sampled rows of one matrix of each shape against the oracle
+    worst = 0.0
+    for m, x, y in mats[:len(shapes)]:
+        blob = m.blob.cpu().numpy()
+        words, tail = tt.unpack_rows(blob, m.M, m.K)
+        rows = np.unique(np.r_[0:4, m.M - 4:m.M, np.linspace(0, m.M - 1, 8).astype(int)])
+        ref, norm = ogemv.gemv_f64(words, m.sigma.cpu().numpy(), tail, x.cpu().numpy(), rows=rows)
+        got = y.cpu().numpy()[:, rows].astype(np.float64)
+        worst = max(worst, float((np.abs(got - ref) / norm).max()))
+    graph = None
+    if not args.no_graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(torch.cuda.current_stream())
+    run = graph.replay if graph is not None else step
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    steps = max(1, args.steps // 4)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / steps
+    flops = sum(2.0 * m.M * m.K * N for m, _, _ in mats)
+    tflops = flops / (ms_step * 1e-3) / 1e12
+    bytes_read = sum(m.read_bytes for m, _, _ in mats)
+    out = {
+        "metric": METRIC, "value": round(bytes_read / (ms_step * 1e-3) / 1e9, 2), "unit": "GB/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16 (MFMA), f32 acc",
+        "data": "synthetic",
+        "config": {"workload": f"prompt of {N} tokens through the Qwen3-{args.model}-shaped linear set x {L} "
+                               f"layers ({len(mats)} Tetra matrices)", "tokens": N, "layers": L,
+                   "hip_graph": graph is not None, "launches_per_step": len(mats)},
+        "tflops": round(tflops, 2),
+        "parity_worst_rel_err": worst,
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_F16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tflops / MFMA_F16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "gemm_kernel", "avg_launch_us": round(ms_step * 1e3 / len(mats), 3),
+                     "flops_per_launch": round(flops / len(mats))},
+    }
+    if not args.no_cpu_baseline:
+        # the oracle on 256-row slices of the first matrices, all tokens, until the time is used
+        t_used, fl = 0.0, 0.0
+        for m, x, _ in mats:
+            if t_used >= args.cpu_seconds:
+                break
+            words, tail = tt.unpack_rows(m.blob.cpu().numpy(), m.M, m.K)
+            sig, xh = m.sigma.cpu().numpy(), x.cpu().numpy()
+            for r0 in range(0, m.M, 256):
+                if t_used >= args.cpu_seconds:
+                    break
+                rows = np.arange(r0, min(r0 + 256, m.M))
+                t0 = time.perf_counter()
+                ogemv.gemv_f64(words, sig, tail, xh, rows=rows)
+                t_used += time.perf_counter() - t0
+                fl += 2.0 * len(rows) * m.K * N
+        out["cpu_baseline"] = {"value": round(fl / t_used / 1e12, 6), "unit": "TFLOP/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{fl / (2 * N) / 1e6:.1f} M weights x {N} tokens in {t_used:.1f} s, "
+                                         "float64 numpy"}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -496,6 +595,8 @@ def main():
         return main_head(args, torch, tt)
     if args.workload == "rotate":
         return main_rotate(args, torch, tt)
+    if args.workload == "prefill":
+        return main_prefill(args, torch, tt)
     stream = torch.cuda.current_stream()
     plan, L, emb = build_workload(torch, tt, args.model, args.layers, args.batch, args.workload)
     torch.cuda.synchronize()
