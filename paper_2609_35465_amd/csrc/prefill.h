@@ -53,10 +53,16 @@ struct PfBlock {
     float s;
 };
 
-// decode this lane's half of a block: lo/hi its word, h its half
-__device__ __forceinline__ PfBlock pf_decode(uint32_t lo, uint32_t hi, int h, lds_bytes* L) {
-    const BlockFetch f = fetch_block(lo, hi, L);
-    __builtin_amdgcn_s_waitcnt(0xC07F);
+// a block's LDS reads in flight: its table entries and this lane's A
+// operands (two 32-token groups, three 8-k steps)
+struct PfFetch {
+    BlockFetch f;
+    half4_t a[2][3];
+};
+
+// finish a block from its table entries: this lane's half of the values (the
+// B operand) and the block scale
+__device__ __forceinline__ PfBlock pf_decode(const BlockFetch& f, int h, lds_bytes* L) {
     const uint32_t ep = f.e ^ (~f.pm & 0xFCFCFCFCu);
     const uint32_t qpair = ~f.pm & 0x3C003C00u;
     PfBlock o;
@@ -64,7 +70,7 @@ __device__ __forceinline__ PfBlock pf_decode(uint32_t lo, uint32_t hi, int h, ld
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk) {
         // coordinates 8 kk + 4h .. 8 kk + 4h + 3: sign group 2 kk + h, row word 2 kk + h
-        const int w = 2 * kk + h;              // h is uniform per half-wave; w is per lane
+        const int w = 2 * kk + h;
         const uint32_t rw = h ? f.r[2 * kk + 1] : f.r[2 * kk];
         const uint32_t sg = rw ^ ((ep << w) & 0x80808080u);
         const uint32_t p0 = pk_add(cvt_pair<false>(sg), qpair);
@@ -85,6 +91,36 @@ __device__ __forceinline__ PfBlock pf_decode(uint32_t lo, uint32_t hi, int h, ld
 // chunk, k = 24 blk + 8 kk + 4h
 __device__ __forceinline__ half4_t pf_a(const _Float16* s_x, int tok, int blk, int kk, int h) {
     return *reinterpret_cast<const half4_t*>(s_x + tok * kPfXStride + 24 * blk + 8 * kk + 4 * h);
+}
+
+// a full chunk of the workgroup's activations (128 tokens x 96 k) in
+// registers: six 16-byte pieces per thread, loaded while the previous chunk
+// is being used and written to LDS after it
+constexpr int kPfPieces = kPfTokens * (kPfChunk / 8) / kPfThreads;
+static_assert(kPfPieces * kPfThreads == kPfTokens * (kPfChunk / 8), "whole pieces per thread");
+
+struct PfXRegs {
+    uint4 v[kPfPieces];
+};
+
+__device__ __forceinline__ void pf_load_x(PfXRegs& r, const GemmArgs& a, int n0, int k0) {
+#pragma unroll
+    for (int i = 0; i < kPfPieces; ++i) {
+        const int idx = static_cast<int>(threadIdx.x) + i * kPfThreads;
+        const int tok = idx / (kPfChunk / 8), q = idx - tok * (kPfChunk / 8);
+        const int n = min(n0 + tok, a.N - 1);                 // rows past N are loaded from row N-1, then zeroed
+        r.v[i] = *reinterpret_cast<const uint4*>(a.x + static_cast<size_t>(n) * a.K + k0 + 8 * q);
+        if (n0 + tok >= a.N) r.v[i] = make_uint4(0, 0, 0, 0);
+    }
+}
+
+__device__ __forceinline__ void pf_store_x(_Float16* s_x, const PfXRegs& r) {
+#pragma unroll
+    for (int i = 0; i < kPfPieces; ++i) {
+        const int idx = static_cast<int>(threadIdx.x) + i * kPfThreads;
+        const int tok = idx / (kPfChunk / 8), q = idx - tok * (kPfChunk / 8);
+        *reinterpret_cast<uint4*>(s_x + tok * kPfXStride + 8 * q) = r.v[i];
+    }
 }
 
 // activations of the workgroup's tokens for k0 .. k0 + cols - 1 into LDS
@@ -119,41 +155,83 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[tg][e] = 0.f;
 
-    auto run_block = [&](uint32_t lo, uint32_t hi, int blk) {
-        const PfBlock pb = pf_decode(lo, hi, h, L);
+    auto issue = [&](uint32_t lo, uint32_t hi, int blk, PfFetch& pf) {
+        pf.f = fetch_block(lo, hi, L);
 #pragma unroll
-        for (int tg = 0; tg < 2; ++tg) {
-            float16_t p;
+        for (int tg = 0; tg < 2; ++tg)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) p[e] = 0.f;
+            for (int kk = 0; kk < 3; ++kk) pf.a[tg][kk] = pf_a(s_x, tok0 + 32 * tg + jr, blk, kk, h);
+    };
+    // blocks 0 .. nb-1 of the staged chunk (words lo[k], hi[k]) as a pipeline:
+    // while a block's products run on the matrix cores, the next block's LDS
+    // reads are in flight and its values are formed on the vector unit
+    auto run_chunk = [&](const uint32_t (&lo)[4], const uint32_t (&hi)[4], int nb) {
+        PfFetch nx;
+        issue(lo[0], hi[0], 0, nx);
+        PfBlock cur = pf_decode(nx.f, h, L);
+        half4_t a[2][3];
+#pragma unroll
+        for (int tg = 0; tg < 2; ++tg)
+#pragma unroll
+            for (int kk = 0; kk < 3; ++kk) a[tg][kk] = nx.a[tg][kk];
+        for (int blk = 0; blk < nb; ++blk) {
+            const bool more = blk + 1 < nb;
+            if (more) issue(lo[min(blk + 1, 3)], hi[min(blk + 1, 3)], blk + 1, nx);
+            float16_t p[2];
+#pragma unroll
+            for (int tg = 0; tg < 2; ++tg) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) p[tg][e] = 0.f;
+            }
 #pragma unroll
             for (int kk = 0; kk < 3; ++kk)
-                p = __builtin_amdgcn_mfma_f32_32x32x8f16(pf_a(s_x, tok0 + 32 * tg + jr, blk, kk, h), pb.b[kk], p,
-                                                         0, 0, 0);
 #pragma unroll
-            for (int e = 0; e < 16; ++e) acc[tg][e] = fmaf(pb.s, p[e], acc[tg][e]);
+                for (int tg = 0; tg < 2; ++tg)
+                    p[tg] = __builtin_amdgcn_mfma_f32_32x32x8f16(a[tg][kk], cur.b[kk], p[tg], 0, 0, 0);
+            PfBlock nxt;
+            if (more) nxt = pf_decode(nx.f, h, L);
+#pragma unroll
+            for (int tg = 0; tg < 2; ++tg)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[tg][e] = fmaf(cur.s, p[tg][e], acc[tg][e]);
+            if (more) {
+                cur = nxt;
+#pragma unroll
+                for (int tg = 0; tg < 2; ++tg)
+#pragma unroll
+                    for (int kk = 0; kk < 3; ++kk) a[tg][kk] = nx.a[tg][kk];
+            }
         }
     };
 
-    for (int g = 0; g < a.ng; ++g) {
-        const uint8_t* gp = tb + static_cast<size_t>(g) * tetra::kGroupBytes;
-        const uint4 lo = *reinterpret_cast<const uint4*>(gp + 16 * rin);
-        const uint2 hi = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * rin);
-        __syncthreads();                                  // the previous chunk has been read
-        pf_stage_x(s_x, a, n0, kPfChunk * g, kPfChunk);
-        __syncthreads();
-        run_block(lo.x, hi.x, 0);
-        run_block(lo.y, hi.x >> 16, 1);
-        run_block(lo.z, hi.y, 2);
-        run_block(lo.w, hi.y >> 16, 3);
+    // whole chunks: the next chunk's activations and code words are loaded
+    // into registers while the current one runs
+    if (a.ng > 0) {
+        PfXRegs xr;
+        pf_load_x(xr, a, n0, 0);
+        uint4 l4 = *reinterpret_cast<const uint4*>(tb + 16 * rin);
+        uint2 h2 = *reinterpret_cast<const uint2*>(tb + 1024 + 8 * rin);
+        for (int g = 0; g < a.ng; ++g) {
+            __syncthreads();                              // the previous chunk has been read
+            pf_store_x(s_x, xr);
+            __syncthreads();
+            const uint32_t lo[4] = {l4.x, l4.y, l4.z, l4.w};
+            const uint32_t hi[4] = {h2.x, h2.x >> 16, h2.y, h2.y >> 16};
+            if (g + 1 < a.ng) {
+                const uint8_t* gp = tb + static_cast<size_t>(g + 1) * tetra::kGroupBytes;
+                pf_load_x(xr, a, n0, kPfChunk * (g + 1));
+                l4 = *reinterpret_cast<const uint4*>(gp + 16 * rin);
+                h2 = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * rin);
+            }
+            run_chunk(lo, hi, 4);
+        }
     }
     if (a.rem > 0) {
-        // the trailing columns: same words as the GEMV's trailing item, for
-        // this lane's row (load_trailing reads the row of lane_now(), which is
-        // rin only in wave 0; read the words of row rin directly here)
-        uint32_t lo[3], hi[3];
+        // the trailing columns: the words of row rin (word_loc gives them for
+        // any lane's row)
+        uint32_t lo[4], hi[4];
 #pragma unroll
-        for (int k = 0; k < 3; ++k) {
+        for (int k = 0; k < 4; ++k) {
             const tetra::WordLoc at = tetra::word_loc(a.nblk, rin, 4 * a.ng + min(k, a.rem - 1));
             lo[k] = *reinterpret_cast<const uint32_t*>(tb + at.lo_off);
             hi[k] = *reinterpret_cast<const uint16_t*>(tb + at.hi_off);
@@ -161,7 +239,7 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
         __syncthreads();
         pf_stage_x(s_x, a, n0, kPfChunk * a.ng, 24 * a.rem);
         __syncthreads();
-        for (int k = 0; k < a.rem; ++k) run_block(lo[k], hi[k], k);
+        run_chunk(lo, hi, a.rem);
     }
     // epilogue: sigma and the unquantised tail; this lane's row and 16 tokens
     // per group
