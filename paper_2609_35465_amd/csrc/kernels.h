@@ -250,10 +250,10 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
 // contiguous range [floor(w Tot / W), floor((w+1) Tot / W)): every wave gets
 // the same number of blocks to within one, whatever the shapes.  A range
 // covers whole tiles and at most two pieces of tiles.  A whole tile is
-// finished by its wave (row scale, unquantised tail, store of y); the waves
-// holding pieces of one tile store their partial sums to the workspace and
-// count themselves in on the tile's counter, and the last one to arrive adds
-// the pieces in wave order, finishes the tile and resets the counter.  The
+// finished by its wave (row scale, unquantised tail, store of y).  The
+// pieces of a tile are combined in two levels (gemv_kernel): in LDS among
+// the waves of a workgroup, then through the per-device workspace among
+// workgroups, each time by the last to count in, in a fixed order.  The
 // ranges depend only on the shapes and W, never on timing or on the batch,
 // so the result is deterministic and row b of a batch-B product is the
 // batch-1 product of x_b bit for bit.
@@ -261,10 +261,11 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
 // Inside its range a wave runs the blocks as a pipeline: the table reads and
 // activation loads of the next block are issued before the current block's
 // arithmetic, the current block's scale read is consumed one block later,
-// and the code words of the next group of four columns are loaded one group
-// ahead, so a wave waits at most once per block.  The activation pairs of a
-// block column are the same for all lanes and come through the scalar unit
-// as SGPR operands of v_dot2_f32_f16.
+// and the code words of whole groups of four columns are loaded one group
+// ahead, so a wave waits at most once per block; a tile's trailing columns
+// run after the groups (run_piece).  The activation pairs of a block column
+// are the same for all lanes and come through the scalar unit as SGPR
+// operands of v_dot2_f32_f16.
 
 struct GemvProblem {
     const uint8_t* codes;

@@ -1,6 +1,7 @@
 // Tetra decode and fused decode-GEMV for MI355X (gfx950): the C ABI of
 // include/tetra.h.  Host code here validates arguments, uploads the decoder
-// tables once per device and launches the kernels of kernels.h.
+// tables once per device and launches the kernels of kernels.h and
+// prefill.h.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
