@@ -23,15 +23,16 @@
  * Memory: all buffers are owned by the caller.  "host" arguments are plain
  * host pointers; "device" arguments are device pointers on the current HIP
  * device (for example from hipMalloc or torch.empty(..., device="cuda")).
- * The library owns its constant decoder tables and one GEMV workspace per
- * device (a counter and two partial sums per workgroup, about 3 MB on a
- * 256-CU part), both set up on the first call on the device (thread-safe;
- * make that first call outside stream capture).  After that, launching calls
- * are asynchronous on the given stream, never synchronise and never
- * allocate.  The workspace is shared by the GEMV calls of a device: GEMV
- * calls on one device must not overlap in time (issue them on one stream,
- * or order the streams); the counters return to zero at the end of every
- * launch.
+ * The library owns its constant decoder tables and two workspaces per
+ * device: the GEMV's (a counter and two partial sums per workgroup, about
+ * 3 MB on a 256-CU part) and tetra_gemm's (a counter and two 32 KB partial
+ * sums per workgroup, about 32 MB), all set up on the first call on the
+ * device (thread-safe; make that first call outside stream capture).  After
+ * that, launching calls are asynchronous on the given stream, never
+ * synchronise and never allocate.  A workspace is shared by the calls of a
+ * device that use it: such calls on one device must not overlap in time
+ * (issue them on one stream, or order the streams); the counters return to
+ * zero at the end of every launch.
  *
  * Errors: every call validates its arguments before any launch and returns
  * a tetra_status.  TETRA_EDEVICE reports a HIP error seen at launch time;
@@ -192,10 +193,14 @@ int tetra_decode(const void* words, size_t n, int8_t* y_out, float* blk_scale_ou
  *   codes / row_scales as in tetra_gemv (16-byte aligned codes)
  *   x: device fp16 [N][K], 16-byte aligned; K must be a multiple of 8
  *   y: device fp32 [N][M], fully overwritten
- * N >= 1 (up to 65535 * 128).  Meant for N well above TETRA_MAX_BATCH; the
- * rounding differs from tetra_gemv's (another summation order), within the
- * same bound.  Asynchronous; TETRA_EINVAL / TETRA_EALIGN / TETRA_EDEVICE as
- * for tetra_gemv.
+ * N >= 1; a prompt whose activations pass 2 GiB runs as several launches.
+ * Meant for N well above TETRA_MAX_BATCH; the rounding differs from
+ * tetra_gemv's (another summation order), within the same bound, and the
+ * split of the work over workgroups follows M, K, N and the CU count, so a
+ * token's result can change in the last bits with N (it never changes from
+ * run to run).  Uses the device's product workspace: like GEMV calls, calls
+ * on one device must not overlap in time.  Asynchronous; TETRA_EINVAL /
+ * TETRA_EALIGN / TETRA_EDEVICE as for tetra_gemv.
  */
 int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
                hipStream_t stream);

@@ -22,6 +22,9 @@ HIP_FLAGS = [
     "-shared",
     # packed FP32 VALU ops stay off on this target
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core results in ordinary VGPRs: the many-token product scales
+    # every block's products on the vector unit, which cannot read AGPRs
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall",
     "-Wno-unused-command-line-argument",
 ]

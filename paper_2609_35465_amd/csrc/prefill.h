@@ -24,6 +24,16 @@
 // tokens (two 64-token halves, two 32-token MFMA groups per wave).  The
 // activations of the 128 tokens go through LDS in chunks of 96 k (one group
 // of four block columns), the decoder tables are staged as in the GEMV.
+//
+// Work split: an item is a (64-row tile, 128-token group) pair and a unit is
+// one chunk of an item (the trailing block columns of a row make one more,
+// shorter unit).  A fixed number of workgroups (two per CU) take equal
+// contiguous ranges of the items' units, so no launch leaves most of the
+// chip idle in a last partial wave of workgroups, however many tiles and
+// tokens there are.  An item whose units span several workgroups is combined
+// as in the GEMV: each publishes its sums through the per-device workspace
+// and the last to count in adds the pieces in workgroup order, which makes
+// the result independent of timing.
 #pragma once
 
 namespace tetra_dev {
@@ -33,6 +43,10 @@ constexpr int kPfWaves = 4;
 constexpr int kPfThreads = kPfWaves * 64;
 constexpr int kPfChunk = 96;               // k per chunk: four blocks
 constexpr int kPfXStride = 104;            // fp16 per token row of the LDS chunk (96 + 8)
+constexpr int kPfGroupsPerCU = 2;          // 2 x 75 KB of LDS, 2 waves per SIMD
+
+constexpr int kPfOut = 32;                 // outputs per thread (one row, 32 tokens)
+constexpr int kPfSlot = kPfThreads * kPfOut;  // floats of one workgroup's piece of an item
 
 struct GemmArgs {
     const uint8_t* codes;
@@ -41,7 +55,39 @@ struct GemmArgs {
     float* y;                              // [N][M]
     unsigned long long tail_off;
     int M, K, N, nblk, T, ng, rem;
+    int tgroups;                           // token groups of kPfTokens
+    int upi;                               // units per item: ng, plus one when rem > 0
+    int workers;                           // workgroups of the launch
+    unsigned long long units;              // items * upi
+    uint32_t* counters;                    // [workers], zero between launches
+    float* partials;                       // [workers][2][kPfSlot]
 };
+
+// workspace of a launch with at most `workers` workgroups
+inline size_t gemm_workspace_bytes(int workers) {
+    return sizeof(uint32_t) * static_cast<size_t>(workers) +
+           sizeof(float) * static_cast<size_t>(workers) * 2 * kPfSlot;
+}
+
+// a workgroup-uniform 64-bit value in scalar registers (the 64-bit divisions
+// below run on the vector unit, which would leave every index derived from
+// them, and the loops they bound, in vector registers)
+__device__ __forceinline__ unsigned long long pf_uniform(unsigned long long v) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+    return (static_cast<unsigned long long>(hi) << 32) | lo;
+}
+
+// first unit of workgroup w's range (w = workers gives the end)
+__device__ __forceinline__ unsigned long long pf_range_begin(int w, const GemmArgs& a) {
+    return pf_uniform(a.units * static_cast<unsigned long long>(w) / static_cast<unsigned long long>(a.workers));
+}
+
+// the workgroup whose range holds unit u
+__device__ __forceinline__ int pf_worker_of(unsigned long long u, const GemmArgs& a) {
+    return __builtin_amdgcn_readfirstlane(
+        static_cast<int>(((u + 1) * static_cast<unsigned long long>(a.workers) - 1) / a.units));
+}
 
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
 typedef float float16_t __attribute__((ext_vector_type(16)));
@@ -93,41 +139,73 @@ __device__ __forceinline__ half4_t pf_a(const _Float16* s_x, int tok, int blk, i
     return *reinterpret_cast<const half4_t*>(s_x + tok * kPfXStride + 24 * blk + 8 * kk + 4 * h);
 }
 
+// this thread's index in the workgroup, read afresh at each use: an index
+// derived from threadIdx once would stay in a register across the whole
+// item loop
+__device__ __forceinline__ int pf_tid() {
+    return (__builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x)) & ~63) | lane_now();
+}
+
 // a full chunk of the workgroup's activations (128 tokens x 96 k) in
 // registers: six 16-byte pieces per thread, loaded while the previous chunk
 // is being used and written to LDS after it
 constexpr int kPfPieces = kPfTokens * (kPfChunk / 8) / kPfThreads;
 static_assert(kPfPieces * kPfThreads == kPfTokens * (kPfChunk / 8), "whole pieces per thread");
 
+// one 24-dword vector rather than an array of six uint4: the array form was
+// placed in scratch memory across the item loop
+typedef uint32_t pf_u24 __attribute__((ext_vector_type(4 * kPfPieces)));
 struct PfXRegs {
-    uint4 v[kPfPieces];
+    pf_u24 v;
 };
 
-__device__ __forceinline__ void pf_load_x(PfXRegs& r, const GemmArgs& a, int n0, int k0) {
+// where this thread's pieces of every chunk of an item come from and go to:
+// piece i is 16 bytes of token tok_i at k offset 8 q_i of the chunk.  Byte
+// offsets from x for chunk 0 (32-bit: the entry point keeps N K 2 below
+// 2^31) and into the LDS chunk.  Tokens past N read row N-1: their products
+// only reach outputs that are never stored.
+struct PfXMap {
+    uint32_t g[kPfPieces];
+    uint32_t l[kPfPieces];
+};
+
+__device__ __forceinline__ PfXMap pf_map(const GemmArgs& a, int n0) {
+    PfXMap m;
+    const int t = pf_tid();
 #pragma unroll
     for (int i = 0; i < kPfPieces; ++i) {
-        const int idx = static_cast<int>(threadIdx.x) + i * kPfThreads;
+        const int idx = t + i * kPfThreads;
         const int tok = idx / (kPfChunk / 8), q = idx - tok * (kPfChunk / 8);
-        const int n = min(n0 + tok, a.N - 1);                 // rows past N are loaded from row N-1, then zeroed
-        r.v[i] = *reinterpret_cast<const uint4*>(a.x + static_cast<size_t>(n) * a.K + k0 + 8 * q);
-        if (n0 + tok >= a.N) r.v[i] = make_uint4(0, 0, 0, 0);
+        m.g[i] = static_cast<uint32_t>(min(n0 + tok, a.N - 1)) * static_cast<uint32_t>(2 * a.K) + 16u * q;
+        m.l[i] = static_cast<uint32_t>(tok * (2 * kPfXStride) + 16 * q);
+    }
+    return m;
+}
+
+__device__ __forceinline__ void pf_load_x(PfXRegs& r, const GemmArgs& a, const PfXMap& m, int k0) {
+    const uint8_t* base = reinterpret_cast<const uint8_t*>(a.x + k0);
+#pragma unroll
+    for (int i = 0; i < kPfPieces; ++i) {
+        const uint4 t = *reinterpret_cast<const uint4*>(base + m.g[i]);
+        r.v[4 * i] = t.x;
+        r.v[4 * i + 1] = t.y;
+        r.v[4 * i + 2] = t.z;
+        r.v[4 * i + 3] = t.w;
     }
 }
 
-__device__ __forceinline__ void pf_store_x(_Float16* s_x, const PfXRegs& r) {
+__device__ __forceinline__ void pf_store_x(_Float16* s_x, const PfXRegs& r, const PfXMap& m) {
 #pragma unroll
-    for (int i = 0; i < kPfPieces; ++i) {
-        const int idx = static_cast<int>(threadIdx.x) + i * kPfThreads;
-        const int tok = idx / (kPfChunk / 8), q = idx - tok * (kPfChunk / 8);
-        *reinterpret_cast<uint4*>(s_x + tok * kPfXStride + 8 * q) = r.v[i];
-    }
+    for (int i = 0; i < kPfPieces; ++i)
+        *reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(s_x) + m.l[i]) =
+            make_uint4(r.v[4 * i], r.v[4 * i + 1], r.v[4 * i + 2], r.v[4 * i + 3]);
 }
 
 // activations of the workgroup's tokens for k0 .. k0 + cols - 1 into LDS
 // (zero for tokens past N); cols is a multiple of 8 and at most 96
 __device__ __forceinline__ void pf_stage_x(_Float16* s_x, const GemmArgs& a, int n0, int k0, int cols) {
     const int per_tok = cols / 8;                        // 16-byte pieces per token
-    for (int i = threadIdx.x; i < kPfTokens * per_tok; i += kPfThreads) {
+    for (int i = pf_tid(); i < kPfTokens * per_tok; i += kPfThreads) {
         const int tok = i / per_tok, q = i - tok * per_tok;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (n0 + tok < a.N)
@@ -139,21 +217,16 @@ __device__ __forceinline__ void pf_stage_x(_Float16* s_x, const GemmArgs& a, int
 __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
     __shared__ uint4 s_tab[kPackedTableBytes / 16];
     __shared__ __attribute__((aligned(16))) _Float16 s_x[kPfTokens * kPfXStride];
+    __shared__ uint32_t s_arrived;
     stage_packed_tables<kPfThreads>(s_tab);
     lds_bytes* L = (lds_bytes*)(s_tab);
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int h = lane >> 5, jr = lane & 31;
-    const int tile = blockIdx.x;
-    const int n0 = blockIdx.y * kPfTokens;
     const int rin = (wave & 1) * 32 + jr;                 // row in the 64-row tile
     const int tok0 = (wave >> 1) * 64;                    // first of the wave's 64 tokens in the chunk
-    const uint8_t* tb = a.codes + static_cast<size_t>(tile) * a.nblk * kChunk;
+    const int w = blockIdx.x;
     float16_t acc[2];
-#pragma unroll
-    for (int tg = 0; tg < 2; ++tg)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[tg][e] = 0.f;
 
     auto issue = [&](uint32_t lo, uint32_t hi, int blk, PfFetch& pf) {
         pf.f = fetch_block(lo, hi, L);
@@ -203,76 +276,164 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
             }
         }
     };
+    // sigma and the unquantised tail applied to an item's sums v; this lane's
+    // row and 16 tokens per group
+    auto finish = [&](const float16_t (&v)[2], int tile, int n0) {
+        // lane indices read afresh: derived from threadIdx they would be
+        // computed once for all items and held in registers throughout
+        const int ln = lane_now();
+        const int fh = ln >> 5;
+        const int frin = (__builtin_amdgcn_readfirstlane(threadIdx.x) & 64) / 2 + (ln & 31);
+        const int ftok0 = (__builtin_amdgcn_readfirstlane(threadIdx.x) & 128) / 2;
+        __syncthreads();
+        // the tail columns of the tokens' activations, 4 bytes at a time (T is even)
+        for (int i = pf_tid(); i < kPfTokens * (a.T >> 1); i += kPfThreads) {
+            const int tok = i / (a.T >> 1), q = i - tok * (a.T >> 1);
+            uint32_t xv = 0;
+            if (n0 + tok < a.N)
+                xv = *reinterpret_cast<const uint32_t*>(a.x + static_cast<size_t>(n0 + tok) * a.K + 24 * a.nblk +
+                                                        2 * q);
+            *reinterpret_cast<uint32_t*>(s_x + tok * kPfXStride + 2 * q) = xv;
+        }
+        __syncthreads();
+        const int row = tile * kTile + frin;
+        if (row < a.M) {
+            const float sg = f16(a.sigma[row]);
+            const uint32_t* tl =
+                reinterpret_cast<const uint32_t*>(a.codes + a.tail_off) + static_cast<size_t>(row) * (a.T >> 1);
+            uint32_t tv[11];
+#pragma unroll
+            for (int q = 0; q < 11; ++q) tv[q] = 2 * q < a.T ? tl[q] : 0u;
+#pragma unroll
+            for (int tg = 0; tg < 2; ++tg)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int tok = ftok0 + 32 * tg + 8 * (e >> 2) + 4 * fh + (e & 3);
+                    if (n0 + tok >= a.N) continue;
+                    const uint32_t* xt = reinterpret_cast<const uint32_t*>(s_x + tok * kPfXStride);
+                    float ts = 0.f;
+#pragma unroll
+                    for (int q = 0; q < 11; ++q)
+                        if (2 * q < a.T) ts = dot2(tv[q], xt[q], ts);
+                    a.y[static_cast<size_t>(n0 + tok) * a.M + row] = fmaf(sg, v[tg][e], ts);
+                }
+        }
+    };
 
-    // whole chunks: the next chunk's activations and code words are loaded
-    // into registers while the current one runs
-    if (a.ng > 0) {
-        PfXRegs xr;
-        pf_load_x(xr, a, n0, 0);
-        uint4 l4 = *reinterpret_cast<const uint4*>(tb + 16 * rin);
-        uint2 h2 = *reinterpret_cast<const uint2*>(tb + 1024 + 8 * rin);
-        for (int g = 0; g < a.ng; ++g) {
-            __syncthreads();                              // the previous chunk has been read
-            pf_store_x(s_x, xr);
-            __syncthreads();
-            const uint32_t lo[4] = {l4.x, l4.y, l4.z, l4.w};
-            const uint32_t hi[4] = {h2.x, h2.x >> 16, h2.y, h2.y >> 16};
-            if (g + 1 < a.ng) {
-                const uint8_t* gp = tb + static_cast<size_t>(g + 1) * tetra::kGroupBytes;
-                pf_load_x(xr, a, n0, kPfChunk * (g + 1));
-                l4 = *reinterpret_cast<const uint4*>(gp + 16 * rin);
-                h2 = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * rin);
+    const unsigned long long u0 = pf_range_begin(w, a), u1 = pf_range_begin(w + 1, a);
+    for (unsigned long long base = pf_uniform(u0 - u0 % a.upi); base < u1; base += a.upi) {
+        // this workgroup's units c0 .. c1-1 of the item starting at unit base
+        const int item = __builtin_amdgcn_readfirstlane(static_cast<int>(base / a.upi));
+        const int c0 = __builtin_amdgcn_readfirstlane(static_cast<int>((u0 > base ? u0 : base) - base));
+        const int c1 = __builtin_amdgcn_readfirstlane(static_cast<int>((u1 < base + a.upi ? u1 : base + a.upi) - base));
+        const int tile = item / a.tgroups;
+        const int n0 = (item - tile * a.tgroups) * kPfTokens;
+        const uint8_t* tb = a.codes + static_cast<size_t>(tile) * a.nblk * kChunk;
+#pragma unroll
+        for (int tg = 0; tg < 2; ++tg)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[tg][e] = 0.f;
+
+        // whole chunks: the next chunk's activations and code words are loaded
+        // into registers while the current one runs
+        const int g1 = min(c1, a.ng);
+        if (c0 < g1) {
+            const PfXMap xm = pf_map(a, n0);
+            PfXRegs xr;
+            pf_load_x(xr, a, xm, kPfChunk * c0);
+            const uint8_t* gp0 = tb + static_cast<size_t>(c0) * tetra::kGroupBytes;
+            uint4 l4 = *reinterpret_cast<const uint4*>(gp0 + 16 * rin);
+            uint2 h2 = *reinterpret_cast<const uint2*>(gp0 + 1024 + 8 * rin);
+            for (int g = c0; g < g1; ++g) {
+                __syncthreads();                          // the previous chunk has been read
+                pf_store_x(s_x, xr, xm);
+                __syncthreads();
+                const uint32_t lo[4] = {l4.x, l4.y, l4.z, l4.w};
+                const uint32_t hi[4] = {h2.x, h2.x >> 16, h2.y, h2.y >> 16};
+                if (g + 1 < g1) {
+                    const uint8_t* gp = tb + static_cast<size_t>(g + 1) * tetra::kGroupBytes;
+                    pf_load_x(xr, a, xm, kPfChunk * (g + 1));
+                    l4 = *reinterpret_cast<const uint4*>(gp + 16 * rin);
+                    h2 = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * rin);
+                }
+                run_chunk(lo, hi, 4);
             }
-            run_chunk(lo, hi, 4);
         }
-    }
-    if (a.rem > 0) {
-        // the trailing columns: the words of row rin (word_loc gives them for
-        // any lane's row)
-        uint32_t lo[4], hi[4];
+        if (a.rem > 0 && c1 == a.upi) {
+            // the trailing columns: the words of row rin (word_loc gives them for
+            // any lane's row)
+            uint32_t lo[4], hi[4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const tetra::WordLoc at = tetra::word_loc(a.nblk, rin, 4 * a.ng + min(k, a.rem - 1));
-            lo[k] = *reinterpret_cast<const uint32_t*>(tb + at.lo_off);
-            hi[k] = *reinterpret_cast<const uint16_t*>(tb + at.hi_off);
+            for (int k = 0; k < 4; ++k) {
+                const tetra::WordLoc at = tetra::word_loc(a.nblk, rin, 4 * a.ng + min(k, a.rem - 1));
+                lo[k] = *reinterpret_cast<const uint32_t*>(tb + at.lo_off);
+                hi[k] = *reinterpret_cast<const uint16_t*>(tb + at.hi_off);
+            }
+            __syncthreads();
+            pf_stage_x(s_x, a, n0, kPfChunk * a.ng, 24 * a.rem);
+            __syncthreads();
+            run_chunk(lo, hi, a.rem);
         }
+        if (c0 == 0 && c1 == a.upi) {
+            finish(acc, tile, n0);
+            continue;
+        }
+
+        // a piece of an item that other workgroups share.  Slot 0 of a workgroup
+        // holds the piece of the item where its range starts, slot 1 that of
+        // the item where it ends.  The sums and the counters are accessed only
+        // with device-scope atomics, coherent across the chip's L2 caches; the
+        // wait orders each thread's sums before the barrier and the count.
+        float* mine = a.partials + (static_cast<size_t>(w) * 2 + (u0 >= base ? 0 : 1)) * kPfSlot + pf_tid();
+#pragma unroll
+        for (int tg = 0; tg < 2; ++tg)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                __hip_atomic_store(mine + (16 * tg + e) * kPfThreads, acc[tg][e], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+        const int wf = pf_worker_of(base, a), wl = pf_worker_of(base + a.upi - 1, a);
         __syncthreads();
-        pf_stage_x(s_x, a, n0, kPfChunk * a.ng, 24 * a.rem);
+        if (threadIdx.x == 0)
+            s_arrived = __hip_atomic_fetch_add(a.counters + wf, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __syncthreads();
-        run_chunk(lo, hi, a.rem);
-    }
-    // epilogue: sigma and the unquantised tail; this lane's row and 16 tokens
-    // per group
-    __syncthreads();
-    // the tail columns of the tokens' activations, 4 bytes at a time (T is even)
-    for (int i = threadIdx.x; i < kPfTokens * (a.T >> 1); i += kPfThreads) {
-        const int tok = i / (a.T >> 1), q = i - tok * (a.T >> 1);
-        uint32_t v = 0;
-        if (n0 + tok < a.N)
-            v = *reinterpret_cast<const uint32_t*>(a.x + static_cast<size_t>(n0 + tok) * a.K + 24 * a.nblk + 2 * q);
-        *reinterpret_cast<uint32_t*>(s_x + tok * kPfXStride + 2 * q) = v;
-    }
-    __syncthreads();
-    const int row = tile * kTile + rin;
-    if (row >= a.M) return;
-    const float sg = f16(a.sigma[row]);
-    const uint32_t* tl = reinterpret_cast<const uint32_t*>(a.codes + a.tail_off) + static_cast<size_t>(row) * (a.T >> 1);
-    uint32_t tv[11];
+        if (s_arrived != static_cast<uint32_t>(wl - wf)) continue;
+        // the last piece in: add all of them in workgroup order, two at a time
+        const int side_wf = pf_range_begin(wf, a) >= base ? 0 : 1;
+        float16_t tot[2];
 #pragma unroll
-    for (int q = 0; q < 11; ++q) tv[q] = 2 * q < a.T ? tl[q] : 0u;
+        for (int tg = 0; tg < 2; ++tg)
 #pragma unroll
-    for (int tg = 0; tg < 2; ++tg)
+            for (int e = 0; e < 16; ++e) tot[tg][e] = 0.f;
+        for (int v0 = wf; v0 <= wl; v0 += 2) {
+            float16_t pv[2][2];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int tok = tok0 + 32 * tg + 8 * (e >> 2) + 4 * h + (e & 3);
-            if (n0 + tok >= a.N) continue;
-            const uint32_t* xt = reinterpret_cast<const uint32_t*>(s_x + tok * kPfXStride);
-            float ts = 0.f;
+            for (int u = 0; u < 2; ++u) {
+                const int v = v0 + u;
+                if (v <= wl && v != w) {
+                    const float* src =
+                        a.partials + (static_cast<size_t>(v) * 2 + (v > wf ? 0 : side_wf)) * kPfSlot + pf_tid();
 #pragma unroll
-            for (int q = 0; q < 11; ++q)
-                if (2 * q < a.T) ts = dot2(tv[q], xt[q], ts);
-            a.y[static_cast<size_t>(n0 + tok) * a.M + row] = fmaf(sg, acc[tg][e], ts);
+                    for (int tg = 0; tg < 2; ++tg)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e)
+                            pv[u][tg][e] = __hip_atomic_load(src + (16 * tg + e) * kPfThreads, __ATOMIC_RELAXED,
+                                                             __HIP_MEMORY_SCOPE_AGENT);
+                } else {
+#pragma unroll
+                    for (int tg = 0; tg < 2; ++tg) pv[u][tg] = acc[tg];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                if (v0 + u <= wl) {
+#pragma unroll
+                    for (int tg = 0; tg < 2; ++tg) tot[tg] += pv[u][tg];
+                }
         }
+        if (threadIdx.x == 0) __hip_atomic_store(a.counters + wf, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        finish(tot, tile, n0);
+    }
 }
 
 }  // namespace tetra_dev

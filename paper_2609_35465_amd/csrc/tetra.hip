@@ -28,13 +28,16 @@ constexpr int kMaxDevices = 64;
 std::mutex g_init_mu;
 bool g_init_done[kMaxDevices];
 
-// Per-device GEMV workspace (tile counters and partial sums of pieces of
-// tiles), allocated and zeroed with the tables; the counters are back at
-// zero after every launch.
+// Per-device workspaces of the GEMV and of the many-token product (counters
+// and partial sums of pieces of tiles or items), allocated and zeroed with the
+// tables; the counters are back at zero after every launch.
 struct Workspace {
     uint32_t* counters = nullptr;
     float* partials = nullptr;
     int max_waves = 0;
+    uint32_t* gemm_counters = nullptr;
+    float* gemm_partials = nullptr;
+    int gemm_workers = 0;
 };
 Workspace g_ws[kMaxDevices];
 
@@ -80,6 +83,17 @@ int ensure_tables(int* dev_out) {
     }
     ws.counters = static_cast<uint32_t*>(mem);
     ws.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(mem) + sizeof(uint32_t) * max_groups);
+    ws.gemm_workers = num_cus(dev) * tetra_dev::kPfGroupsPerCU;
+    const size_t gemm_bytes = tetra_dev::gemm_workspace_bytes(ws.gemm_workers);
+    void* gmem = nullptr;
+    if (hipMalloc(&gmem, gemm_bytes) != hipSuccess) return TETRA_EDEVICE;
+    if (hipMemset(gmem, 0, gemm_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+        (void)hipFree(gmem);
+        return TETRA_EDEVICE;
+    }
+    ws.gemm_counters = static_cast<uint32_t*>(gmem);
+    ws.gemm_partials =
+        reinterpret_cast<float*>(static_cast<uint8_t*>(gmem) + sizeof(uint32_t) * static_cast<size_t>(ws.gemm_workers));
     g_init_done[dev] = true;
     return TETRA_OK;
 }
@@ -348,18 +362,16 @@ int tetra_head4_gemv(const void* q, const uint16_t* scale_off, const uint16_t* x
     return int4_gemv_launch<tetra_dev::kHead4Group>(q, scale_off, x, y, rows, dim, batch, stream);
 }
 
-int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
-               hipStream_t stream) {
-    if (!codes || !row_scales || !x || !y || M < 1 || K < 24 || N < 1 || K % 8) return TETRA_EINVAL;
-    if (!aligned(codes, 16) || !aligned(x, 16) || !aligned(row_scales, 2) || !aligned(y, 4)) return TETRA_EALIGN;
+namespace {
+
+// one launch of the many-token product over tokens n_base .. n_base + N - 1
+int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
+                const Shape& s, const Workspace& ws, hipStream_t stream) {
     const long long token_groups = (static_cast<long long>(N) + tetra_dev::kPfTokens - 1) / tetra_dev::kPfTokens;
-    if (token_groups > 65535) return TETRA_EINVAL;
-    int dev;
-    if (int st = ensure_tables(&dev)) return st;
-    Shape s;
-    if (!shape_of(M, K, &s)) return TETRA_EINVAL;
+    const long long items = static_cast<long long>(s.tiles) * token_groups;
+    if (items >= (1ll << 31)) return TETRA_EINVAL;
     tetra_dev::GemmArgs a;
-    a.codes = static_cast<const uint8_t*>(codes);
+    a.codes = codes;
     a.sigma = row_scales;
     a.x = x;
     a.y = y;
@@ -371,9 +383,40 @@ int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x,
     a.T = s.T;
     a.ng = s.nblk / tetra::kGroupCols;
     a.rem = s.nblk % tetra::kGroupCols;
-    hipLaunchKernelGGL(tetra_dev::gemm_kernel, dim3(static_cast<unsigned>(s.tiles), static_cast<unsigned>(token_groups)),
-                       dim3(tetra_dev::kPfThreads), 0, stream, a);
+    a.tgroups = static_cast<int>(token_groups);
+    a.upi = a.ng + (a.rem > 0 ? 1 : 0);
+    a.units = static_cast<unsigned long long>(items) * static_cast<unsigned long long>(a.upi);
+    a.workers = static_cast<int>(std::min<unsigned long long>(a.units, static_cast<unsigned long long>(ws.gemm_workers)));
+    if (a.units > ~0ull / static_cast<unsigned long long>(a.workers + 1)) return TETRA_EINVAL;   // range arithmetic
+    a.counters = ws.gemm_counters;
+    a.partials = ws.gemm_partials;
+    hipLaunchKernelGGL(tetra_dev::gemm_kernel, dim3(static_cast<unsigned>(a.workers)), dim3(tetra_dev::kPfThreads), 0,
+                       stream, a);
     return launch_status();
+}
+
+}  // namespace
+
+int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
+               hipStream_t stream) {
+    if (!codes || !row_scales || !x || !y || M < 1 || K < 24 || N < 1 || K % 8) return TETRA_EINVAL;
+    if (!aligned(codes, 16) || !aligned(x, 16) || !aligned(row_scales, 2) || !aligned(y, 4)) return TETRA_EALIGN;
+    int dev;
+    if (int st = ensure_tables(&dev)) return st;
+    Shape s;
+    if (!shape_of(M, K, &s)) return TETRA_EINVAL;
+    // the kernel addresses a launch's activations with 32-bit byte offsets:
+    // prompts longer than that run as several launches of whole token groups
+    const long long slice = std::max<long long>(
+        tetra_dev::kPfTokens,
+        ((0x7FFFFFFFll / (2ll * K)) / tetra_dev::kPfTokens) * tetra_dev::kPfTokens);
+    for (long long n = 0; n < N; n += slice) {
+        const int cnt = static_cast<int>(std::min<long long>(slice, N - n));
+        if (int st = gemm_launch(static_cast<const uint8_t*>(codes), row_scales, x + n * K, y + n * M, M, K, cnt, s,
+                                 g_ws[dev], stream))
+            return st;
+    }
+    return TETRA_OK;
 }
 
 int tetra_rotate(const uint16_t* x, const uint8_t* sign_bits, uint16_t* out, int K, int n, int rows,

@@ -551,7 +551,7 @@ def test_gemm_token_tiles(N):
     _check_gemm(pk, workloads.activations(N, N, K), label="tokens")
 
 
-@pytest.mark.parametrize("name", ["q", "gate", "down"])
+@pytest.mark.parametrize("name", ["q", "k", "gate", "down"])
 def test_gemm_14b_shapes_sampled(name):
     shapes = {n: (M, K) for n, M, K in workloads.layer_shapes("14B")}
     M, K = shapes[name]
@@ -559,3 +559,31 @@ def test_gemm_14b_shapes_sampled(name):
     pk = Packed(words, sigma, tail, K)
     rng = np.random.default_rng(77 + len(name))
     _check_gemm(pk, workloads.activations(len(name), 203, K), rows=_sample_rows(M, rng, n=96), label=name)
+
+
+@pytest.mark.parametrize("M,K,N", [(1024, 5120, 203), (200, 1536, 1), (4096, 2400, 129)])
+def test_gemm_split_items_repeat_bitwise(M, K, N):
+    """Items cut across workgroups (16 pieces each for 1024 x 5120 at 203 tokens,
+    one unit per workgroup for 200 x 1536 at one token): two calls in a row,
+    with a GEMV on the same device between them, give the same bits, so the
+    piece counters are back at zero after each launch and the pieces are
+    added in a fixed order."""
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(0, 7) + M + N, M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(M + N, N, K)
+    rng = np.random.default_rng(5 + N)
+    first = _check_gemm(pk, x, rows=_sample_rows(M, rng, n=64), label="split")
+    y = torch.empty((N, M), dtype=torch.float32, device="cuda")
+    yv = torch.empty((1, M), dtype=torch.float32, device="cuda")
+    xd = _f16_dev(x)
+    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N)
+    tt.gemv(pk.blob, pk.sigma, xd[:1], yv, M, K, 1)
+    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N)
+    torch.cuda.synchronize()
+    again = y.cpu().numpy()
+    rows = _sample_rows(M, np.random.default_rng(5 + N), n=64)
+    assert np.array_equal(again[:, rows], first)
+    y2 = torch.empty((N, M), dtype=torch.float32, device="cuda")
+    tt.gemm(pk.blob, pk.sigma, xd, y2, M, K, N)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
