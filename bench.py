@@ -52,7 +52,7 @@ def parse():
                     help="matrix: one launch per matrix; deps: per layer [q,k,v] [o] "
                          "[gate,up] [down] (the launches a decode step can fuse); "
                          "layer: one grouped launch per layer")
-    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4", "head", "rotate", "prefill"],
+    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4", "head", "rotate", "prefill", "encode"],
                     help="tetra: every projection a Tetra matrix (the GEMV metric); c4: the "
                          "full decode step -- 10%% of the projections (seeded) stored as int4 "
                          "w4g128 and one 4-bit embedding row gathered per step; head: the "
@@ -569,6 +569,76 @@ def main_prefill(args, torch, tt):
     return 0
 
 
+ENCODE_BLOCKS = 20000
+VALU32_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12      # 32-bit vector lane operations per second, in T
+
+
+def main_encode(args, torch, tt):
+    """The encoder on the paper's retention workload: 20,000 Gaussian blocks of
+    24 weights (unit variance, row scale 1), two trial radii, one launch."""
+    from oracle import encoder as oencoder
+    n = ENCODE_BLOCKS
+    rng = np.random.default_rng(0x7E7A_0080)
+    w = rng.standard_normal((n, 24)).astype(np.float32)
+    wd = torch.from_numpy(w).cuda()
+    sd = torch.ones(n, dtype=torch.float32, device="cuda")
+    out = torch.zeros(3 * n, dtype=torch.int16, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def run():
+        tt.encode(wd, sd, n, out, stream=stream.cuda_stream)
+
+    run()
+    torch.cuda.synchronize()
+    b = out.cpu().numpy().view(np.uint16).reshape(n, 3).astype(np.uint64)
+    words = b[:, 0] | (b[:, 1] << np.uint64(16)) | (b[:, 2] << np.uint64(32))
+    rec = oencoder.reconstruct(words, np.ones(n))
+    mse = float(((w.astype(np.float64) - rec) ** 2).mean())
+    # parity: sampled blocks against the oracle, word for word
+    idx = rng.choice(n, 4, replace=False)
+    mism = int((oencoder.encode_blocks(w[idx], 1.0, tt.ENCODE_RADII) != words[idx]).sum())
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    steps = max(1, args.steps // 4)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / steps
+    # algorithmic work: every (p, pattern byte) pair scores every row of each
+    # section's lists (4096 + 2048 + 4096 rows) with 8 additions, per trial radius
+    adds = 2.0 * 256 * (4096 + 2048 + 4096) * 8 * n
+    tops = adds / (ms_step * 1e-3) / 1e12
+    out_j = {
+        "metric": "Tetra encoder throughput, 24-weight blocks per second", "value": round(n / (ms_step * 1e-3), 1),
+        "unit": "blocks/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "i32 scores, f64 choices",
+        "data": "synthetic",
+        "config": {"workload": f"{n} Gaussian blocks of 24 weights, radii {tt.ENCODE_RADII[0]:g} and "
+                               f"{tt.ENCODE_RADII[1]:g}", "blocks": n},
+        "retention": round(oencoder.retention(mse), 5), "mse_per_weight": round(mse, 6),
+        "parity_sampled_mismatches": mism,
+        "roofline": {"bound": "alu", "achieved": round(tops, 3), "peak": round(VALU32_PEAK_TOPS, 1),
+                     "unit": "Tops/s", "frac": round(tops / VALU32_PEAK_TOPS, 4), "traffic": None,
+                     "kernel": "encode_kernel", "avg_launch_us": round(ms_step * 1e3, 1),
+                     "ops_per_launch": adds},
+    }
+    if not args.no_cpu_baseline:
+        t_used, done = 0.0, 0
+        while t_used < min(args.cpu_seconds, 15.0) and done < n:
+            t0 = time.perf_counter()
+            oencoder.encode_block(w[done], 1.0, tt.ENCODE_RADII)
+            t_used += time.perf_counter() - t0
+            done += 1
+        out_j["cpu_baseline"] = {"value": round(done / t_used, 3), "unit": "blocks/s", "cores": 1, "kind": "oracle",
+                                 "sample": f"the first {done} blocks in {t_used:.1f} s, numpy"}
+    print(json.dumps(out_j), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -597,6 +667,8 @@ def main():
         return main_rotate(args, torch, tt)
     if args.workload == "prefill":
         return main_prefill(args, torch, tt)
+    if args.workload == "encode":
+        return main_encode(args, torch, tt)
     stream = torch.cuda.current_stream()
     plan, L, emb = build_workload(torch, tt, args.model, args.layers, args.batch, args.workload)
     torch.cuda.synchronize()

@@ -206,6 +206,27 @@ int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x,
                hipStream_t stream);
 
 /*
+ * Encoder of 24-weight blocks (the offline step of Sec. 3.1, shape-gain of
+ * Eq. 2): for each block the canonical word of the kept lattice point whose
+ * direction is closest among the nearest kept points to r * w / ||w|| at
+ * the two trial radii r = radius0, radius1, and the gain bit nearest to the
+ * block's projection on it.  Scores are exact integers (targets on a grid of
+ * 2^-16, see the design notes for the full definition and its tie rules), so
+ * the result is fixed by the inputs.  A block whose squared norm is zero or
+ * not finite gets the word 0.
+ *   w:         device fp32 [n][24], block order (coordinate j of a block
+ *              multiplies activation 24 blk + j), 4-byte aligned
+ *   sigma:     device fp32 [n], the row scale of each block's row
+ *   words_out: device, n * 6 bytes, canonical little-endian words, 2-byte
+ *              aligned (the input format of tetra_decode)
+ *   radius0, radius1: in (0, 25]
+ * Asynchronous.  TETRA_EINVAL for NULL pointers, n == 0 or a radius out of
+ * range; TETRA_EALIGN; TETRA_EDEVICE at launch.
+ */
+int tetra_encode(const float* w, const float* sigma, size_t n, double radius0, double radius1, void* words_out,
+                 hipStream_t stream);
+
+/*
  * Dense reconstruction of a packed matrix (Eq. 2), for testing:
  *   w_out[row][24*blk+j] = fl32(fl32(y_j * s_blk) * sigma_row),
  *   w_out[row][24*nblk+t] = tail[row][t].

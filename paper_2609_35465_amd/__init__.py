@@ -20,6 +20,8 @@ ROW_TILE = 64
 TABLE_BLOB_BYTES = 18824
 MAX_BATCH = 8
 MAX_GROUP = 16
+ENCODE_MAX_RADIUS = 25.0
+ENCODE_RADII = (13.0, 15.0)        # trial radii of the encoder: the best integer pair on Gaussian blocks
 
 _vp, _sz, _int = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
 
@@ -40,6 +42,7 @@ _SIGNATURES = {
     "tetra_rotate": (_int, [_vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_gemm": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_emb4_gather": (_int, [_vp, _vp, _int, _int, _vp, _int, _vp, _vp]),
+    "tetra_encode": (_int, [_vp, _vp, _sz, ctypes.c_double, ctypes.c_double, _vp, _vp]),
 }
 EXPORTED = tuple(_SIGNATURES)
 
@@ -145,6 +148,15 @@ def gemm(codes, row_scales, x, y, M: int, K: int, N: int, stream=None):
     """y[N, M] = W x for N activation rows (a prompt), on the matrix cores."""
     _check(_call("tetra_gemm", _ptr(codes), _ptr(row_scales), _ptr(x), _ptr(y), M, K, N, _stream(stream)),
            "tetra_gemm")
+
+
+def encode(w, sigma, n: int, words_out, radii=None, stream=None):
+    """Canonical words [n][6 bytes] of n blocks w [n, 24] (float32, block
+    order) with per-block scales sigma [n] (float32): the nearest kept point
+    at two trial radii, then the gain bit."""
+    r0, r1 = ENCODE_RADII if radii is None else radii
+    _check(_call("tetra_encode", _ptr(w), _ptr(sigma), n, float(r0), float(r1), _ptr(words_out), _stream(stream)),
+           "tetra_encode")
 
 
 class Problem(ctypes.Structure):

@@ -1,9 +1,10 @@
 // Tetra decode and fused decode-GEMV for MI355X (gfx950): the C ABI of
 // include/tetra.h.  Host code here validates arguments, uploads the decoder
-// tables once per device and launches the kernels of kernels.h and
-// prefill.h.
+// tables once per device and launches the kernels of kernels.h, prefill.h
+// and encoder.h.
 #include <hip/hip_runtime.h>
 
+#include <climits>
 #include <cmath>
 
 #include <algorithm>
@@ -15,6 +16,7 @@
 #include "device_tables.h"
 #include "kernels.h"
 #include "prefill.h"
+#include "encoder.h"
 #include "tables.h"
 #include "word_format.h"
 
@@ -417,6 +419,27 @@ int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x,
             return st;
     }
     return TETRA_OK;
+}
+
+int tetra_encode(const float* w, const float* sigma, size_t n, double radius0, double radius1, void* words_out,
+                 hipStream_t stream) {
+    if (!w || !sigma || !words_out || n == 0) return TETRA_EINVAL;
+    for (double r : {radius0, radius1})
+        if (!(r > 0.0 && r <= tetra_dev::kEncMaxRadius)) return TETRA_EINVAL;
+    if (!aligned(w, 4) || !aligned(sigma, 4) || !aligned(words_out, 2)) return TETRA_EALIGN;
+    int dev;
+    if (int st = ensure_tables(&dev)) return st;
+    tetra_dev::EncodeArgs a;
+    a.w = w;
+    a.sigma = sigma;
+    a.words = static_cast<uint16_t*>(words_out);
+    a.n = n;
+    a.alpha[0] = radius0;
+    a.alpha[1] = radius1;
+    const size_t grid = std::min<size_t>(n, static_cast<size_t>(num_cus(dev)) * 8);
+    hipLaunchKernelGGL(tetra_dev::encode_kernel, dim3(static_cast<unsigned>(grid)), dim3(tetra_dev::kEncThreads), 0,
+                       stream, a);
+    return launch_status();
 }
 
 int tetra_rotate(const uint16_t* x, const uint8_t* sign_bits, uint16_t* out, int K, int n, int rows,

@@ -587,3 +587,82 @@ def test_gemm_split_items_repeat_bitwise(M, K, N):
     tt.gemm(pk.blob, pk.sigma, xd, y2, M, K, N)
     torch.cuda.synchronize()
     assert torch.equal(y, y2)
+
+
+# ----------------------------------------------------------------- encoder
+
+from oracle import codec as ocodec, encoder as oencoder, tables as otables  # noqa: E402
+
+
+def _encode_gpu(w, sigma, radii=None):
+    """Words (uint64) of blocks w [n, 24] through tetra_encode."""
+    n = w.shape[0]
+    wd = torch.from_numpy(np.ascontiguousarray(w, dtype=np.float32)).cuda()
+    sd = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(sigma, (n,)), dtype=np.float32)).cuda()
+    out = torch.zeros(3 * n, dtype=torch.int16, device="cuda")
+    tt.encode(wd, sd, n, out, radii=radii)
+    torch.cuda.synchronize()
+    b = out.cpu().numpy().view(np.uint16).reshape(n, 3).astype(np.uint64)
+    return b[:, 0] | (b[:, 1] << np.uint64(16)) | (b[:, 2] << np.uint64(32))
+
+
+def test_encode_matches_oracle():
+    """Word for word against the oracle, with degenerate blocks: zero, NaN,
+    infinite, norms near 1e-30 and 1e30, a block exactly along a decoded
+    point, one dominant coordinate; per-block row scales."""
+    rng = np.random.default_rng(31)
+    w = rng.standard_normal((16, 24)).astype(np.float32)
+    w[1] = 0.0
+    w[2] *= np.float32(1e-30)
+    w[3] *= np.float32(1e30)
+    w[4, 5] = np.nan
+    w[5, 0] = np.inf
+    y = ocodec.decode(np.array([0x5A5A12345678], dtype=np.uint64))[0][0].astype(np.float32)
+    w[6] = y / np.linalg.norm(y) * np.float32(4.9)
+    w[7] = np.float32(0.01) * w[7]
+    w[7, 11] = 3.0
+    sigma = rng.uniform(0.5, 2.0, 16).astype(np.float32)
+    got = _encode_gpu(w, sigma)
+    want = oencoder.encode_blocks(w, sigma, tt.ENCODE_RADII)
+    print(f"[encode] blocks={len(w)} mismatches={(got != want).sum()}", flush=True)
+    assert np.array_equal(got, want)
+    assert got[1] == 0 and got[4] == 0 and got[5] == 0
+
+
+def test_encode_returns_random_words_at_their_radius():
+    """6,000 random words: a block along each decoded point, of norm gain[g]
+    (sigma 1), encoded with both trial radii equal to the point's norm, gives
+    the word back (the property the oracle pins, here at scale)."""
+    rng = np.random.default_rng(8)
+    words = rng.integers(0, 1 << 48, size=6000, dtype=np.uint64)
+    y, m, _ = ocodec.decode(words)
+    y = y.astype(np.float64)
+    g = ocodec.fields(words)["g"]
+    keep = m > 0
+    words, y, m, g = words[keep], y[keep], m[keep], g[keep]
+    ny = np.sqrt(16.0 * m)
+    w = (y * (otables.gain()[g].astype(np.float64) / ny)[:, None]).astype(np.float32)
+    got = np.zeros_like(words)
+    for mv in np.unique(m):
+        sel = m == mv
+        r = float(np.sqrt(16.0 * mv))
+        got[sel] = _encode_gpu(w[sel], np.ones(sel.sum(), np.float32), radii=(r, r))
+    print(f"[encode round trip] words={len(words)} mismatches={(got != words).sum()}", flush=True)
+    assert np.array_equal(got, words)
+
+
+def test_encode_retention_gaussian_blocks():
+    """20,000 Gaussian blocks (the paper's retention workload): the error of
+    y / ||y|| gain[g] sigma against the blocks, as retention of the 2 bits per
+    weight spent, and six sampled blocks against the oracle."""
+    rng = np.random.default_rng(88)
+    n = 20000
+    w = rng.standard_normal((n, 24)).astype(np.float32)
+    words = _encode_gpu(w, np.ones(n, np.float32))
+    rec = oencoder.reconstruct(words, np.ones(n))
+    D = float(((w.astype(np.float64) - rec) ** 2).mean())
+    ret = oencoder.retention(D)
+    print(f"[encode retention] blocks={n} mse={D:.5f} retention={100 * ret:.2f} % (paper: 88.80 %)", flush=True)
+    assert 0.85 <= ret <= 0.92
+    idx = rng.choice(n, 6, replace=False)
+    assert np.array_equal(words[idx], oencoder.encode_blocks(w[idx], 1.0, tt.ENCODE_RADII))

@@ -235,4 +235,11 @@ def test_int4_head4_and_emb4_validation():
     assert lib.tetra_emb4_gather(fake, fake, 0, 128, fake, 1, fake, None) == tt.EINVAL
     assert lib.tetra_emb4_gather(fake, fake, 10, 128, fake, 0, fake, None) == tt.EINVAL
     assert lib.tetra_emb4_gather(fake, fake, 10, 128, fake + 2, 1, fake, None) == tt.EALIGN
+    assert lib.tetra_encode(None, fake, 4, 14.0, 17.0, fake, None) == tt.EINVAL
+    assert lib.tetra_encode(fake, fake, 0, 14.0, 17.0, fake, None) == tt.EINVAL
+    assert lib.tetra_encode(fake, fake, 4, 0.0, 17.0, fake, None) == tt.EINVAL          # radius <= 0
+    assert lib.tetra_encode(fake, fake, 4, 14.0, 25.5, fake, None) == tt.EINVAL         # radius > 25
+    assert lib.tetra_encode(fake, fake, 4, float("nan"), 17.0, fake, None) == tt.EINVAL
+    assert lib.tetra_encode(fake + 2, fake, 4, 14.0, 17.0, fake, None) == tt.EALIGN
+    assert lib.tetra_encode(fake, fake, 4, 14.0, 17.0, fake + 1, None) == tt.EALIGN
 

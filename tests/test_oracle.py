@@ -498,3 +498,85 @@ def test_rotation_pins():
     want = np.array([(-1) ** bin(i & 5).count("1") for i in range(n)]) / np.sqrt(n)
     assert np.allclose(full[:n], want, rtol=1e-15)
     assert not full[n:].any()                                       # blocks do not mix
+
+
+# ----------------------------------------------------------------- encoder
+
+from oracle import encoder  # noqa: E402
+
+
+def _block_of(word):
+    """A block pointing exactly at the decoded point of `word`, with norm
+    gain[g] (sigma = 1), and that point's radius."""
+    y = codec.decode(np.array([word], dtype=np.uint64))[0][0].astype(np.int64)
+    g = int(codec.fields(np.array([word], dtype=np.uint64))["g"][0])
+    ny = float(np.sqrt((y * y).sum()))
+    return (y * (float(tables.gain()[g]) / ny)).astype(np.float32), ny
+
+
+def test_encoder_returns_the_word_at_its_own_radius():
+    """At a trial radius equal to ||y|| the targets are y itself (on the
+    2^-16 grid), every other kept point scores strictly lower, and the gain
+    nearest to ||w|| = gain[g] is g: the search must give back the word,
+    every field of every section included (both row halves, the middle list
+    on both sides of N0, all trellis edges)."""
+    rng = np.random.default_rng(2024)
+    words = [int(v) for v in rng.integers(0, 1 << 48, size=6, dtype=np.uint64)]
+    # a word with delta = 1 (middle index past N0) and one with delta = 0
+    f = codec.fields(np.array(words, dtype=np.uint64))
+    assert (f["i2"] >= tables.rank_table()["n0"]).any() and (f["i2"] < tables.rank_table()["n0"]).any()
+    for wd in words:
+        w, ny = _block_of(wd)
+        assert encoder.encode_block(w, 1.0, [ny]) == wd
+        # a second, worse radius does not displace the exact direction
+        assert encoder.encode_block(w, 1.0, [ny, 0.5 * ny]) == wd
+
+
+def test_encoder_search_beats_every_single_field_change():
+    """The search result scores at least as high as every word that differs
+    from it in one field: each row index over its whole list (a brute force
+    of each section given the others), each trellis edge and state, p and
+    r; and at least as high as 20,000 random words."""
+    rng = np.random.default_rng(99)
+    w = rng.standard_normal(24).astype(np.float32)
+    T = encoder.targets(w, 14.0)
+    best, f, y = encoder.nearest_point(T)
+    assert encoder.score(T, y) == best
+    word = int(codec.pack_fields(g=0, **f))
+    assert np.array_equal(codec.decode(np.array([word], dtype=np.uint64))[0][0], y)
+    sweeps = {"i1": 2048, "i2": 2048, "i3": 2048, "s8": 64, "b1": 2, "b2": 16, "b3": 2, "p": 2, "r": 2}
+    for name, n in sweeps.items():
+        ff = dict(f, g=0)
+        ff[name] = np.arange(n)
+        ff = {k: np.broadcast_to(np.asarray(v), (n,)) for k, v in ff.items()}
+        ys = codec.decode(codec.pack_fields(**ff))[0].astype(np.int64)
+        scores = (2 * T[None] * ys - encoder.SCALE * ys * ys).sum(axis=1)
+        assert scores.max() <= best, name
+        assert scores[f[name]] == best, name
+    ys = codec.decode(rng.integers(0, 1 << 48, size=20000, dtype=np.uint64))[0].astype(np.int64)
+    assert ((2 * T[None] * ys - encoder.SCALE * ys * ys).sum(axis=1) <= best).all()
+
+
+def test_encoder_degenerate_blocks_and_gain_rule():
+    """Zero and non-finite blocks give the word 0; a block along a decoded
+    point but longer than both gains takes the larger gain, shorter than
+    both the smaller one."""
+    assert encoder.encode_block(np.zeros(24, np.float32), 1.0, [14.0, 17.0]) == 0
+    bad = np.zeros(24, np.float32)
+    bad[3] = np.nan
+    assert encoder.encode_block(bad, 1.0, [14.0, 17.0]) == 0
+    bad[3] = np.inf
+    assert encoder.encode_block(bad, 1.0, [14.0, 17.0]) == 0
+    rng = np.random.default_rng(5)
+    wd = int(rng.integers(0, 1 << 48, dtype=np.uint64))
+    w, ny = _block_of(wd)
+    g = [int(codec.fields(np.array([encoder.encode_block(w * s, 1.0, [ny])], np.uint64))["g"][0])
+         for s in (0.5, 10.0)]
+    assert g == [0, 1]
+
+
+def test_retention_formula():
+    """0.5 log2(1 / D) bits of the Gaussian limit over the 2 bits spent:
+    D = 2^-4 is a rate of 2 bits, retention 1; D = 1/4 gives 1/2."""
+    assert encoder.retention(2.0 ** -4) == pytest.approx(1.0)
+    assert encoder.retention(0.25) == pytest.approx(0.5)
