@@ -176,20 +176,30 @@ __device__ __forceinline__ uint32_t block_values(const BlockFetch& f, uint32_t y
 // Decoder tables into LDS: all loads first, then all stores, so that a
 // workgroup pays one memory round trip (NT: threads of the workgroup).  The
 // loads and stores are unconditional, so that none is sunk into a branch: a
-// thread past the end loads and stores the last word again.
+// thread past the end loads and stores the last word again.  The staged
+// words are one vector rather than an array of uint4, which the compiler
+// may place in scratch memory when other loads are in flight beside it.
 template <int NT>
 struct TableStage {
     static constexpr int kN = static_cast<int>(kPackedTableBytes / 16);
     static constexpr int kPer = (kN + NT - 1) / NT;
-    uint4 v[kPer];
+    typedef uint32_t vec_t __attribute__((ext_vector_type(4 * kPer)));
+    vec_t v;
     __device__ __forceinline__ void load() {
         const uint4* src = reinterpret_cast<const uint4*>(&g_packed);
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) v[k] = src[min(static_cast<int>(threadIdx.x) + k * NT, kN - 1)];
+        for (int k = 0; k < kPer; ++k) {
+            const uint4 t = src[min(static_cast<int>(threadIdx.x) + k * NT, kN - 1)];
+            v[4 * k] = t.x;
+            v[4 * k + 1] = t.y;
+            v[4 * k + 2] = t.z;
+            v[4 * k + 3] = t.w;
+        }
     }
     __device__ __forceinline__ void store(uint4* dst) const {
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) dst[min(static_cast<int>(threadIdx.x) + k * NT, kN - 1)] = v[k];
+        for (int k = 0; k < kPer; ++k)
+            dst[min(static_cast<int>(threadIdx.x) + k * NT, kN - 1)] = make_uint4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
     }
 };
 
@@ -496,6 +506,34 @@ __device__ __forceinline__ Piece begin_piece(const GemvProblem& P, int t, int c0
     return pc;
 }
 
+// 2 KB of zeros: the loads of a wave with no piece, or of a piece with no
+// group (or no trailing columns), read here, so that they need no branch.
+// Every offset load_group and load_trailing use is below 1536.
+__device__ __align__(16) uint8_t g_zero_codes[2048];
+
+// begin_piece for the first piece of a wave, with every load unconditional:
+// the loads are issued between the table loads and the table stores, and a
+// branch around them would make the stores wait for them too (the wait
+// counter is not tracked across a join).  `live` is false for a wave past
+// the last; its words are then never used.
+__device__ __forceinline__ Piece begin_piece_live(const GemvProblem& P, int t, int c0, int c1, int lane, bool live) {
+    Piece pc;
+    pc.t = t;
+    pc.c0 = c0;
+    pc.c1 = c1;
+    pc.j = c0 >> 2;
+    pc.jg = min((c1 - 1) >> 2, P.ng - 1);
+    pc.tr = c1 > 4 * P.ng;
+    const uint8_t* tb = P.codes + static_cast<size_t>(t) * P.nblk * kChunk;
+    const bool gok = live && pc.j <= pc.jg;
+    const uint8_t* gb = gok ? tb : g_zero_codes;
+    pc.cw = load_group(gb, gok ? pc.j : 0, lane);
+    pc.nw = load_group(gb, gok ? min(pc.j + 1, pc.jg) : 0, lane);
+    const bool tok = live && pc.tr;
+    pc.tw = load_trailing(tok ? tb : g_zero_codes, tok ? P.ng : 0, tok ? P.rem : 1);
+    return pc;
+}
+
 // blocks kb..ke-1 of item j (words cw; the next item's words nw, column
 // ncol0), whole group or not
 template <int B>
@@ -630,9 +668,8 @@ void gemv_kernel(const GemvGroup grp) {
     const int w0 = g * kGemvWaves;
     const int w = w0 + wid;
     const int wlast = min(w0 + kGemvWaves, W) - 1;
-    stage_packed_tables<kGemvThreads>(s_tab);
-    __syncthreads();
-    if (w >= W) return;
+    TableStage<kGemvThreads> ts;
+    ts.load();
     uint32_t i = __builtin_amdgcn_readfirstlane(range_begin(w, grp));
     const uint32_t end = __builtin_amdgcn_readfirstlane(range_begin(w + 1, grp));
     int p = 0;
@@ -645,7 +682,14 @@ void gemv_kernel(const GemvGroup grp) {
         const uint32_t left = end - i;
         c1 = left < static_cast<uint32_t>(grp.prob[p].nblk - c) ? c + static_cast<int>(left) : grp.prob[p].nblk;
     }
-    Piece pc = begin_piece(grp.prob[p], t, c, c1, lane);
+    // the first piece's code words are requested while the tables arrive;
+    // the barrier orders LDS only, so they stay in flight across it
+    Piece pc = begin_piece_live(grp.prob[p], t, c, c1, lane, w < W);
+    ts.store(s_tab);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+    if (w >= W) return;
     bool first = true;
     for (;;) {
         const GemvProblem& P = grp.prob[p];
