@@ -12,10 +12,13 @@
 // ||w||) the point maximises S(y) = sum_j (2 T_j y_j - 2^16 y_j^2), an exact
 // integer that splits over the three sections of Sec. 3.2:
 //   * a section's score depends on the parity p, its pattern byte P (one of
-//     the 128 even-weight bytes) and its rank row; for each (p, P, class)
-//     the best row of the section's list (Sec. 3.3: the class halves of the
-//     table for sections 1 and 3, the middle list for section 2) is found
-//     by one thread scanning the list, the first of equal scores kept;
+//     the 128 even-weight bytes, named by its low seven bits) and its rank
+//     row; for each (p, P, class) the best row of the section's list
+//     (Sec. 3.3: the class halves of the table for sections 1 and 3, the
+//     middle list for section 2) is kept, the first of equal scores.  A
+//     thread scores one eighth of the rows for eight bytes that differ only
+//     in bits 4-6 (bit 7 is their parity): the eight sums share the first
+//     four coordinates and build on each other over the last four;
 //   * the three are joined over the 4096 trellis paths and the parities r
 //     and delta, with r3 = p xor r xor delta (Eq. 3); equal sums go to the
 //     smallest key (s8 | p << 6 | r << 7 | b1 << 8 | b2 << 9 | b3 << 13) * 2
@@ -49,9 +52,6 @@ __device__ __forceinline__ int enc_value(int o, int rk) {
     return (neg ? -u : u) + (1 - p);
 }
 
-// the even-weight byte whose low seven bits are i
-__device__ __forceinline__ uint32_t enc_even_byte(uint32_t i) { return i | ((__builtin_popcount(i) & 1u) << 7); }
-
 // first (start, length) of the class-c list of section s, in table rows
 __device__ __forceinline__ void enc_list(int s, int c, int* start, int* len) {
     if (s == 1) {
@@ -71,6 +71,8 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(const EncodeArgs a)
     __shared__ int s_E[24 * 4 * 8];                 // [j][o][rank]: 2 T_j v - 2^16 v^2
     __shared__ int s_best[3 * 2 * 128 * 2];         // [s][p][P & 127][c]
     __shared__ short s_arg[3 * 2 * 128 * 2];
+    __shared__ int s_sl_s[8 * 32 * 8];              // [slice][p, low bits][high bits]: best score
+    __shared__ short s_sl_i[8 * 32 * 8];            // and its row in the list
     __shared__ int s_red_s[kEncThreads / 64], s_red_k[kEncThreads / 64];
     __shared__ int s_T[24];
     __shared__ double s_f[2];
@@ -81,9 +83,11 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(const EncodeArgs a)
     }
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
-    // this thread's (p, pattern byte) in the section search
-    const int my_p = t >> 7;
-    const uint32_t my_P = enc_even_byte(static_cast<uint32_t>(t & 127));
+    // this thread's part of the section search: a slice of the rows, the
+    // parity p and the low four bits of the pattern-byte index
+    const int my_slice = t >> 5, my_combo = t & 31;
+    const int my_p = my_combo >> 4, my_lo = my_combo & 15;
+    const int my_par = __builtin_popcount(my_lo) & 1;
     for (size_t blk = blockIdx.x; blk < a.n; blk += gridDim.x) {
         const float* w = a.w + 24 * blk;
         __syncthreads();                            // tables staged; the previous block is done with LDS
@@ -110,32 +114,78 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(const EncodeArgs a)
                 s_E[i] = 2 * s_T[j] * v - kEncScale * v * v;
             }
             __syncthreads();
-            // best row of each section's list per (p, P, class)
+            // best row of each section's list per (p, P, class): thread t scans
+            // slice t / 32 of the list for parity p and the eight pattern bytes
+            // whose index has the low bits of t % 16; the slices then meet in
+            // row order
             for (int sec = 0; sec < 3; ++sec) {
-                const int* E = s_E + 8 * sec * 32;
-                int base[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) base[j] = 32 * j + 8 * (my_p + 2 * static_cast<int>((my_P >> j) & 1u));
+                const int* Ep = s_E + 256 * sec + 8 * my_p;      // E[j][p + 2x][r] at Ep[32 j + 16 x + r]
                 for (int c = 0; c < 2; ++c) {
                     int start, len;
                     enc_list(sec, c, &start, &len);
-                    int bs = INT_MIN, bi = 0;
-                    for (int i = 0; i < len; ++i) {
-                        const uint32_t row = s_rows[start + i];
-                        int sc = 0;
+                    const int i0 = (len * my_slice) >> 3, i1 = (len * (my_slice + 1)) >> 3;
+                    int bs[8], bi[8];
 #pragma unroll
-                        for (int j = 0; j < 8; ++j) sc += E[base[j] + static_cast<int>((row >> (4 * j)) & 15u)];
-                        if (sc > bs) {
-                            bs = sc;
-                            bi = i;
+                    for (int k = 0; k < 8; ++k) {
+                        bs[k] = INT_MIN;
+                        bi[k] = 0;
+                    }
+                    for (int i = i0; i < i1; ++i) {
+                        const uint32_t row = s_rows[start + i];
+                        int r[8];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) r[j] = static_cast<int>((row >> (4 * j)) & 15u);
+                        int base = 0;
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) base += Ep[32 * j + 16 * ((my_lo >> j) & 1) + r[j]];
+                        int e[4][2];
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            e[j][0] = Ep[32 * (4 + j) + r[4 + j]];
+                            e[j][1] = Ep[32 * (4 + j) + 16 + r[4 + j]];
+                        }
+                        // coordinate 7 is the parity bit of the byte
+                        const int f0 = my_par ? e[3][1] : e[3][0];
+                        const int f1 = my_par ? e[3][0] : e[3][1];
+                        int s4[2], s45[4];
+#pragma unroll
+                        for (int a4 = 0; a4 < 2; ++a4) s4[a4] = base + e[0][a4];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) s45[q] = s4[q & 1] + e[1][q >> 1];
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            const int sc = s45[k & 3] + e[2][k >> 2] + ((__builtin_popcount(k) & 1) ? f1 : f0);
+                            if (sc > bs[k]) {
+                                bs[k] = sc;
+                                bi[k] = i;
+                            }
                         }
                     }
-                    const int at = ((sec * 2 + my_p) * 128 + (t & 127)) * 2 + c;
-                    s_best[at] = bs;
-                    s_arg[at] = static_cast<short>(bi);
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        s_sl_s[(my_slice * 32 + my_combo) * 8 + k] = bs[k];
+                        s_sl_i[(my_slice * 32 + my_combo) * 8 + k] = static_cast<short>(bi[k]);
+                    }
+                    __syncthreads();
+                    {
+                        // thread t: combination t / 8, byte k = t % 8, slices in row order
+                        const int cb = t >> 3, k = t & 7;
+                        int ws = INT_MIN, wi = 0;
+                        for (int sl = 0; sl < 8; ++sl) {
+                            const int v = s_sl_s[(sl * 32 + cb) * 8 + k];
+                            if (v > ws) {
+                                ws = v;
+                                wi = s_sl_i[(sl * 32 + cb) * 8 + k];
+                            }
+                        }
+                        const int pp = cb >> 4, i7 = (cb & 15) | (k << 4);
+                        const int at = ((sec * 2 + pp) * 128 + i7) * 2 + c;
+                        s_best[at] = ws;
+                        s_arg[at] = static_cast<short>(wi);
+                    }
+                    __syncthreads();
                 }
             }
-            __syncthreads();
             // join over the trellis: keys t, t + 256, ... in ascending order
             int js = INT_MIN, jk = 0;
             for (int k = t; k < kEncJoinKeys; k += kEncThreads) {
