@@ -25,8 +25,8 @@
  * device (for example from hipMalloc or torch.empty(..., device="cuda")).
  * The library owns its constant decoder tables and two workspaces per
  * device: the GEMV's (a counter and two partial sums per workgroup, about
- * 3 MB on a 256-CU part) and tetra_gemm's (a counter and two 32 KB partial
- * sums per workgroup, about 32 MB), all set up on the first call on the
+ * 3 MB on a 256-CU part) and tetra_gemm's (a counter and two 64 KB partial
+ * sums per workgroup, about 64 MB), all set up on the first call on the
  * device (thread-safe; make that first call outside stream capture).  After
  * that, launching calls are asynchronous on the given stream, never
  * synchronise and never allocate.  A workspace is shared by the calls of a

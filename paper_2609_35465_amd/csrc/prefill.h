@@ -45,8 +45,8 @@ constexpr int kPfChunk = 96;               // k per chunk: four blocks
 constexpr int kPfXStride = 104;            // fp16 per token row of the LDS chunk (96 + 8)
 constexpr int kPfGroupsPerCU = 2;          // 2 x 75 KB of LDS, 2 waves per SIMD
 
-constexpr int kPfOut = 32;                 // outputs per thread (one row, 32 tokens)
-constexpr int kPfSlot = kPfThreads * kPfOut;  // floats of one workgroup's piece of an item
+constexpr int kPfMaxTG = 4;                // 32-token MFMA groups per wave, at most
+constexpr int kPfSlot = kPfThreads * 16 * kPfMaxTG;   // floats of one workgroup's piece of an item
 
 struct GemmArgs {
     const uint8_t* codes;
@@ -56,6 +56,7 @@ struct GemmArgs {
     unsigned long long tail_off;
     int M, K, N, nblk, T, ng, rem;
     int tgroups;                           // token groups of kPfTokens
+    int tiles;                             // 64-row tiles
     int upi;                               // units per item: ng, plus one when rem > 0
     int workers;                           // workgroups of the launch
     unsigned long long units;              // items * upi
@@ -214,6 +215,12 @@ __device__ __forceinline__ void pf_stage_x(_Float16* s_x, const GemmArgs& a, int
     }
 }
 
+// TG = 4: an item is two tiles (128 rows) by 128 tokens and each wave takes
+// 32 rows by all 128 tokens, so that every decoded block feeds four token
+// groups.  TG = 2: an item is one tile by 128 tokens, each wave 32 rows by
+// 64 tokens; items are then half the size, for shapes with few rows, whose
+// items would otherwise be cut into many pieces.
+template <int TG>
 __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
     __shared__ uint4 s_tab[kPackedTableBytes / 16];
     __shared__ __attribute__((aligned(16))) _Float16 s_x[kPfTokens * kPfXStride];
@@ -223,68 +230,92 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int h = lane >> 5, jr = lane & 31;
-    const int rin = (wave & 1) * 32 + jr;                 // row in the 64-row tile
-    const int tok0 = (wave >> 1) * 64;                    // first of the wave's 64 tokens in the chunk
+    const int rin = (wave & 1) * 32 + jr;                 // row in the wave's 64-row tile
+    const int tok0 = TG == 4 ? 0 : (wave >> 1) * 64;      // first of the wave's tokens in the chunk
     const int w = blockIdx.x;
-    float16_t acc[2];
+    float16_t acc[TG];
 
+    // the A operands of 32-token groups tg0, tg0 + 1 for a block
+    auto load_a = [&](int blk, int tg0, half4_t (&av)[2][3]) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int kk = 0; kk < 3; ++kk) av[q][kk] = pf_a(s_x, tok0 + 32 * (tg0 + q) + jr, blk, kk, h);
+    };
     auto issue = [&](uint32_t lo, uint32_t hi, int blk, PfFetch& pf) {
         pf.f = fetch_block(lo, hi, L);
-#pragma unroll
-        for (int tg = 0; tg < 2; ++tg)
-#pragma unroll
-            for (int kk = 0; kk < 3; ++kk) pf.a[tg][kk] = pf_a(s_x, tok0 + 32 * tg + jr, blk, kk, h);
+        load_a(blk, 0, pf.a);
     };
     // blocks 0 .. nb-1 of the staged chunk (words lo[k], hi[k]) as a pipeline:
     // while a block's products run on the matrix cores, the next block's LDS
-    // reads are in flight and its values are formed on the vector unit
+    // reads are in flight and its values are formed on the vector unit.  The
+    // four token groups go in two pairs; the second pair's activations are
+    // read while the first pair's products run.
     auto run_chunk = [&](const uint32_t (&lo)[4], const uint32_t (&hi)[4], int nb) {
         PfFetch nx;
         issue(lo[0], hi[0], 0, nx);
         PfBlock cur = pf_decode(nx.f, h, L);
-        half4_t a[2][3];
+        half4_t a01[2][3];
 #pragma unroll
-        for (int tg = 0; tg < 2; ++tg)
+        for (int q = 0; q < 2; ++q)
 #pragma unroll
-            for (int kk = 0; kk < 3; ++kk) a[tg][kk] = nx.a[tg][kk];
+            for (int kk = 0; kk < 3; ++kk) a01[q][kk] = nx.a[q][kk];
         for (int blk = 0; blk < nb; ++blk) {
             const bool more = blk + 1 < nb;
             if (more) issue(lo[min(blk + 1, 3)], hi[min(blk + 1, 3)], blk + 1, nx);
             float16_t p[2];
 #pragma unroll
-            for (int tg = 0; tg < 2; ++tg) {
+            for (int q = 0; q < 2; ++q) {
 #pragma unroll
-                for (int e = 0; e < 16; ++e) p[tg][e] = 0.f;
+                for (int e = 0; e < 16; ++e) p[q][e] = 0.f;
             }
 #pragma unroll
             for (int kk = 0; kk < 3; ++kk)
 #pragma unroll
-                for (int tg = 0; tg < 2; ++tg)
-                    p[tg] = __builtin_amdgcn_mfma_f32_32x32x8f16(a[tg][kk], cur.b[kk], p[tg], 0, 0, 0);
+                for (int q = 0; q < 2; ++q) p[q] = __builtin_amdgcn_mfma_f32_32x32x8f16(a01[q][kk], cur.b[kk], p[q], 0, 0, 0);
+            half4_t a23[2][3];
+            if constexpr (TG == 4) load_a(blk, 2, a23);
             PfBlock nxt;
             if (more) nxt = pf_decode(nx.f, h, L);
 #pragma unroll
-            for (int tg = 0; tg < 2; ++tg)
+            for (int q = 0; q < 2; ++q)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) acc[tg][e] = fmaf(cur.s, p[tg][e], acc[tg][e]);
+                for (int e = 0; e < 16; ++e) acc[q][e] = fmaf(cur.s, p[q][e], acc[q][e]);
+            if constexpr (TG == 4) {
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) p[q][e] = 0.f;
+                }
+#pragma unroll
+                for (int kk = 0; kk < 3; ++kk)
+#pragma unroll
+                    for (int q = 0; q < 2; ++q)
+                        p[q] = __builtin_amdgcn_mfma_f32_32x32x8f16(a23[q][kk], cur.b[kk], p[q], 0, 0, 0);
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[2 + q][e] = fmaf(cur.s, p[q][e], acc[2 + q][e]);
+            }
             if (more) {
                 cur = nxt;
 #pragma unroll
-                for (int tg = 0; tg < 2; ++tg)
+                for (int q = 0; q < 2; ++q)
 #pragma unroll
-                    for (int kk = 0; kk < 3; ++kk) a[tg][kk] = nx.a[tg][kk];
+                    for (int kk = 0; kk < 3; ++kk) a01[q][kk] = nx.a[q][kk];
             }
         }
     };
-    // sigma and the unquantised tail applied to an item's sums v; this lane's
-    // row and 16 tokens per group
-    auto finish = [&](const float16_t (&v)[2], int tile, int n0) {
+    // sigma and the unquantised tail applied to an item's sums v for the
+    // wave's tile wt (only when it holds rows); this lane's row, 16 tokens per
+    // group
+    auto finish = [&](const float16_t (&v)[TG], int wt, bool live, int n0) {
         // lane indices read afresh: derived from threadIdx they would be
         // computed once for all items and held in registers throughout
         const int ln = lane_now();
         const int fh = ln >> 5;
         const int frin = (__builtin_amdgcn_readfirstlane(threadIdx.x) & 64) / 2 + (ln & 31);
-        const int ftok0 = (__builtin_amdgcn_readfirstlane(threadIdx.x) & 128) / 2;
+        const int ftok0 = TG == 4 ? 0 : (__builtin_amdgcn_readfirstlane(threadIdx.x) & 128) / 2;
         __syncthreads();
         // the tail columns of the tokens' activations, 4 bytes at a time (T is even)
         for (int i = pf_tid(); i < kPfTokens * (a.T >> 1); i += kPfThreads) {
@@ -296,8 +327,8 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
             *reinterpret_cast<uint32_t*>(s_x + tok * kPfXStride + 2 * q) = xv;
         }
         __syncthreads();
-        const int row = tile * kTile + frin;
-        if (row < a.M) {
+        const int row = wt * kTile + frin;
+        if (live && row < a.M) {
             const float sg = f16(a.sigma[row]);
             const uint32_t* tl =
                 reinterpret_cast<const uint32_t*>(a.codes + a.tail_off) + static_cast<size_t>(row) * (a.T >> 1);
@@ -305,7 +336,7 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
 #pragma unroll
             for (int q = 0; q < 11; ++q) tv[q] = 2 * q < a.T ? tl[q] : 0u;
 #pragma unroll
-            for (int tg = 0; tg < 2; ++tg)
+            for (int tg = 0; tg < TG; ++tg)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
                     const int tok = ftok0 + 32 * tg + 8 * (e >> 2) + 4 * fh + (e & 3);
@@ -326,11 +357,18 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
         const int item = __builtin_amdgcn_readfirstlane(static_cast<int>(base / a.upi));
         const int c0 = __builtin_amdgcn_readfirstlane(static_cast<int>((u0 > base ? u0 : base) - base));
         const int c1 = __builtin_amdgcn_readfirstlane(static_cast<int>((u1 < base + a.upi ? u1 : base + a.upi) - base));
-        const int tile = item / a.tgroups;
-        const int n0 = (item - tile * a.tgroups) * kPfTokens;
-        const uint8_t* tb = a.codes + static_cast<size_t>(tile) * a.nblk * kChunk;
+        const int irow = item / a.tgroups;
+        const int n0 = (item - irow * a.tgroups) * kPfTokens;
+        // the wave's tile: with TG = 4 waves 0-1 take the item's first tile and
+        // waves 2-3 the second (past the last tile they repeat it and store
+        // nothing); with TG = 2 all four take the item's tile
+        const int wt_raw =
+            TG == 4 ? 2 * irow + (__builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x)) >> 7) : irow;
+        const bool live = wt_raw < a.tiles;
+        const int wt = min(wt_raw, a.tiles - 1);
+        const uint8_t* tb = a.codes + static_cast<size_t>(wt) * a.nblk * kChunk;
 #pragma unroll
-        for (int tg = 0; tg < 2; ++tg)
+        for (int tg = 0; tg < TG; ++tg)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[tg][e] = 0.f;
 
@@ -375,7 +413,7 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
             run_chunk(lo, hi, a.rem);
         }
         if (c0 == 0 && c1 == a.upi) {
-            finish(acc, tile, n0);
+            finish(acc, wt, live, n0);
             continue;
         }
 
@@ -386,7 +424,7 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
         // wait orders each thread's sums before the barrier and the count.
         float* mine = a.partials + (static_cast<size_t>(w) * 2 + (u0 >= base ? 0 : 1)) * kPfSlot + pf_tid();
 #pragma unroll
-        for (int tg = 0; tg < 2; ++tg)
+        for (int tg = 0; tg < TG; ++tg)
 #pragma unroll
             for (int e = 0; e < 16; ++e)
                 __hip_atomic_store(mine + (16 * tg + e) * kPfThreads, acc[tg][e], __ATOMIC_RELAXED,
@@ -398,41 +436,28 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
             s_arrived = __hip_atomic_fetch_add(a.counters + wf, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __syncthreads();
         if (s_arrived != static_cast<uint32_t>(wl - wf)) continue;
-        // the last piece in: add all of them in workgroup order, two at a time
+        // the last piece in: add all of them in workgroup order (its own piece
+        // too, read back like the others)
         const int side_wf = pf_range_begin(wf, a) >= base ? 0 : 1;
-        float16_t tot[2];
 #pragma unroll
-        for (int tg = 0; tg < 2; ++tg)
+        for (int tg = 0; tg < TG; ++tg)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) tot[tg][e] = 0.f;
-        for (int v0 = wf; v0 <= wl; v0 += 2) {
-            float16_t pv[2][2];
+            for (int e = 0; e < 16; ++e) acc[tg][e] = 0.f;
+        for (int v = wf; v <= wl; ++v) {
+            const float* src =
+                a.partials + (static_cast<size_t>(v) * 2 + (v > wf ? 0 : side_wf)) * kPfSlot + pf_tid();
+            float16_t pv[TG];
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const int v = v0 + u;
-                if (v <= wl && v != w) {
-                    const float* src =
-                        a.partials + (static_cast<size_t>(v) * 2 + (v > wf ? 0 : side_wf)) * kPfSlot + pf_tid();
+            for (int tg = 0; tg < TG; ++tg)
 #pragma unroll
-                    for (int tg = 0; tg < 2; ++tg)
+                for (int e = 0; e < 16; ++e)
+                    pv[tg][e] = __hip_atomic_load(src + (16 * tg + e) * kPfThreads, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
-                        for (int e = 0; e < 16; ++e)
-                            pv[u][tg][e] = __hip_atomic_load(src + (16 * tg + e) * kPfThreads, __ATOMIC_RELAXED,
-                                                             __HIP_MEMORY_SCOPE_AGENT);
-                } else {
-#pragma unroll
-                    for (int tg = 0; tg < 2; ++tg) pv[u][tg] = acc[tg];
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-                if (v0 + u <= wl) {
-#pragma unroll
-                    for (int tg = 0; tg < 2; ++tg) tot[tg] += pv[u][tg];
-                }
+            for (int tg = 0; tg < TG; ++tg) acc[tg] += pv[tg];
         }
         if (threadIdx.x == 0) __hip_atomic_store(a.counters + wf, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        finish(tot, tile, n0);
+        finish(acc, wt, live, n0);
     }
 }
 

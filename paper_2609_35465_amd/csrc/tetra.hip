@@ -370,7 +370,16 @@ namespace {
 int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
                 const Shape& s, const Workspace& ws, hipStream_t stream) {
     const long long token_groups = (static_cast<long long>(N) + tetra_dev::kPfTokens - 1) / tetra_dev::kPfTokens;
-    const long long items = static_cast<long long>(s.tiles) * token_groups;
+    // four token groups per wave (items of two tiles) unless that cuts the
+    // average item into more than eight pieces over the launch's workgroups;
+    // then two (items of one tile)
+    const int upi = s.nblk / tetra::kGroupCols + (s.nblk % tetra::kGroupCols ? 1 : 0);
+    long long items = static_cast<long long>((s.tiles + 1) / 2) * token_groups;
+    int tg = 4;
+    if (std::min<long long>(items * upi, ws.gemm_workers) > 8 * items) {
+        tg = 2;
+        items = static_cast<long long>(s.tiles) * token_groups;
+    }
     if (items >= (1ll << 31)) return TETRA_EINVAL;
     tetra_dev::GemmArgs a;
     a.codes = codes;
@@ -386,14 +395,19 @@ int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t
     a.ng = s.nblk / tetra::kGroupCols;
     a.rem = s.nblk % tetra::kGroupCols;
     a.tgroups = static_cast<int>(token_groups);
-    a.upi = a.ng + (a.rem > 0 ? 1 : 0);
+    a.tiles = s.tiles;
+    a.upi = upi;
     a.units = static_cast<unsigned long long>(items) * static_cast<unsigned long long>(a.upi);
     a.workers = static_cast<int>(std::min<unsigned long long>(a.units, static_cast<unsigned long long>(ws.gemm_workers)));
     if (a.units > ~0ull / static_cast<unsigned long long>(a.workers + 1)) return TETRA_EINVAL;   // range arithmetic
     a.counters = ws.gemm_counters;
     a.partials = ws.gemm_partials;
-    hipLaunchKernelGGL(tetra_dev::gemm_kernel, dim3(static_cast<unsigned>(a.workers)), dim3(tetra_dev::kPfThreads), 0,
-                       stream, a);
+    if (tg == 4)
+        hipLaunchKernelGGL(tetra_dev::gemm_kernel<4>, dim3(static_cast<unsigned>(a.workers)),
+                           dim3(tetra_dev::kPfThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(tetra_dev::gemm_kernel<2>, dim3(static_cast<unsigned>(a.workers)),
+                           dim3(tetra_dev::kPfThreads), 0, stream, a);
     return launch_status();
 }
 

@@ -561,10 +561,12 @@ def test_gemm_14b_shapes_sampled(name):
     _check_gemm(pk, workloads.activations(len(name), 203, K), rows=_sample_rows(M, rng, n=96), label=name)
 
 
-@pytest.mark.parametrize("M,K,N", [(1024, 5120, 203), (200, 1536, 1), (4096, 2400, 129)])
+@pytest.mark.parametrize("M,K,N", [(1024, 5120, 203), (200, 1536, 1), (4096, 2400, 129), (2100, 256, 77)])
 def test_gemm_split_items_repeat_bitwise(M, K, N):
     """Items cut across workgroups (16 pieces each for 1024 x 5120 at 203 tokens,
-    one unit per workgroup for 200 x 1536 at one token): two calls in a row,
+    one unit per workgroup for 200 x 1536 at one token, two-tile items with an
+    odd tile count for 2100 x 256, whose last item has no second tile): two
+    calls in a row,
     with a GEMV on the same device between them, give the same bits, so the
     piece counters are back at zero after each launch and the pieces are
     added in a fixed order."""
