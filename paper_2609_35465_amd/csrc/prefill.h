@@ -62,7 +62,34 @@ struct GemmArgs {
     unsigned long long units;              // items * upi
     uint32_t* counters;                    // [workers], zero between launches
     float* partials;                       // [workers][2][kPfSlot]
+    int partial_bytes;                     // size of the partials array
 };
+
+// pieces go through the workspace in 16-byte buffer accesses with the cache
+// policy of device-scope atomics (coherent across the chip's L2 caches):
+// quad q of a thread's sums at byte 16 (256 q + thread) of its slot
+typedef uint32_t pf_u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kPfCoherent = 16;            // sc1
+constexpr int kPfRsrcWord3 = 0x00020000;   // raw 32-bit buffer, gfx9
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t pf_rsrc(const GemmArgs& a) {
+    return __builtin_amdgcn_make_buffer_rsrc(a.partials, static_cast<short>(0), a.partial_bytes, kPfRsrcWord3);
+}
+
+// Values pass through these helpers by value: __builtin_bit_cast applied
+// directly to a subscript of a vector (acc[tg][i], q[i]) was compiled as a
+// cast of element 0 whatever i was.
+__device__ __forceinline__ uint32_t pf_bits(float f) { return __builtin_bit_cast(uint32_t, f); }
+__device__ __forceinline__ float pf_float(uint32_t u) { return __builtin_bit_cast(float, u); }
+
+// component i (a constant) of a quad
+__device__ __forceinline__ uint32_t pf_part(const pf_u32x4& v, int i) {
+    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+__device__ __forceinline__ uint32_t pf_slot_bytes(int worker, int side) {
+    return static_cast<uint32_t>((worker * 2 + side) * kPfSlot) * 4u;
+}
 
 // workspace of a launch with at most `workers` workgroups
 inline size_t gemm_workspace_bytes(int workers) {
@@ -422,13 +449,19 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
         // the item where it ends.  The sums and the counters are accessed only
         // with device-scope atomics, coherent across the chip's L2 caches; the
         // wait orders each thread's sums before the barrier and the count.
-        float* mine = a.partials + (static_cast<size_t>(w) * 2 + (u0 >= base ? 0 : 1)) * kPfSlot + pf_tid();
+        const __amdgpu_buffer_rsrc_t rs = pf_rsrc(a);
+        {
+            const uint32_t mine = pf_slot_bytes(w, u0 >= base ? 0 : 1) + 16u * static_cast<uint32_t>(pf_tid());
 #pragma unroll
-        for (int tg = 0; tg < TG; ++tg)
+            for (int tg = 0; tg < TG; ++tg)
 #pragma unroll
-            for (int e = 0; e < 16; ++e)
-                __hip_atomic_store(mine + (16 * tg + e) * kPfThreads, acc[tg][e], __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
+                for (int k = 0; k < 4; ++k) {
+                    const pf_u32x4 q = {pf_bits(acc[tg][4 * k]), pf_bits(acc[tg][4 * k + 1]),
+                                        pf_bits(acc[tg][4 * k + 2]), pf_bits(acc[tg][4 * k + 3])};
+                    __builtin_amdgcn_raw_buffer_store_b128(q, rs, mine + 16u * kPfThreads * (4 * tg + k), 0,
+                                                           kPfCoherent);
+                }
+        }
         __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
         const int wf = pf_worker_of(base, a), wl = pf_worker_of(base + a.upi - 1, a);
         __syncthreads();
@@ -437,24 +470,32 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
         __syncthreads();
         if (s_arrived != static_cast<uint32_t>(wl - wf)) continue;
         // the last piece in: add all of them in workgroup order (its own piece
-        // too, read back like the others)
+        // too, read back like the others), PB pieces per round trip
+        constexpr int PB = TG == 4 ? 2 : 4;
         const int side_wf = pf_range_begin(wf, a) >= base ? 0 : 1;
 #pragma unroll
         for (int tg = 0; tg < TG; ++tg)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[tg][e] = 0.f;
-        for (int v = wf; v <= wl; ++v) {
-            const float* src =
-                a.partials + (static_cast<size_t>(v) * 2 + (v > wf ? 0 : side_wf)) * kPfSlot + pf_tid();
-            float16_t pv[TG];
+        for (int v0 = wf; v0 <= wl; v0 += PB) {
+            pf_u32x4 pv[PB][4 * TG];
 #pragma unroll
-            for (int tg = 0; tg < TG; ++tg)
+            for (int u = 0; u < PB; ++u) {
+                const int v = min(v0 + u, wl);          // past the last: the last again, not added
+                const uint32_t src = pf_slot_bytes(v, v > wf ? 0 : side_wf) + 16u * static_cast<uint32_t>(pf_tid());
 #pragma unroll
-                for (int e = 0; e < 16; ++e)
-                    pv[tg][e] = __hip_atomic_load(src + (16 * tg + e) * kPfThreads, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
+                for (int q = 0; q < 4 * TG; ++q)
+                    pv[u][q] = __builtin_amdgcn_raw_buffer_load_b128(rs, src + 16u * kPfThreads * q, 0, kPfCoherent);
+            }
 #pragma unroll
-            for (int tg = 0; tg < TG; ++tg) acc[tg] += pv[tg];
+            for (int u = 0; u < PB; ++u)
+                if (v0 + u <= wl) {
+#pragma unroll
+                    for (int tg = 0; tg < TG; ++tg)
+#pragma unroll
+                        for (int e = 0; e < 16; ++e)
+                            acc[tg][e] += pf_float(pf_part(pv[u][4 * tg + (e >> 2)], e & 3));
+                }
         }
         if (threadIdx.x == 0) __hip_atomic_store(a.counters + wf, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         finish(acc, wt, live, n0);

@@ -402,6 +402,7 @@ int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t
     if (a.units > ~0ull / static_cast<unsigned long long>(a.workers + 1)) return TETRA_EINVAL;   // range arithmetic
     a.counters = ws.gemm_counters;
     a.partials = ws.gemm_partials;
+    a.partial_bytes = static_cast<int>(sizeof(float) * 2 * tetra_dev::kPfSlot * static_cast<size_t>(ws.gemm_workers));
     if (tg == 4)
         hipLaunchKernelGGL(tetra_dev::gemm_kernel<4>, dim3(static_cast<unsigned>(a.workers)),
                            dim3(tetra_dev::kPfThreads), 0, stream, a);
