@@ -398,7 +398,11 @@ int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t
     a.tiles = s.tiles;
     a.upi = upi;
     a.units = static_cast<unsigned long long>(items) * static_cast<unsigned long long>(a.upi);
-    a.workers = static_cast<int>(std::min<unsigned long long>(a.units, static_cast<unsigned long long>(ws.gemm_workers)));
+    // at most eight workgroups per item on average: past that, a few more
+    // chunks per workgroup cost less than the longer reduction
+    a.workers = static_cast<int>(std::min<unsigned long long>(
+        std::min<unsigned long long>(a.units, static_cast<unsigned long long>(ws.gemm_workers)),
+        static_cast<unsigned long long>(items) * 8));
     if (a.units > ~0ull / static_cast<unsigned long long>(a.workers + 1)) return TETRA_EINVAL;   // range arithmetic
     a.counters = ws.gemm_counters;
     a.partials = ws.gemm_partials;
