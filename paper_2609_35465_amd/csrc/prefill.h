@@ -20,20 +20,22 @@
 // row's block scale, which then scales all 16 outputs of the lane (one row,
 // 16 tokens).
 //
-// A workgroup of 4 waves covers one 64-row tile (two 32-row halves) and 128
-// tokens (two 64-token halves, two 32-token MFMA groups per wave).  The
-// activations of the 128 tokens go through LDS in chunks of 96 k (one group
-// of four block columns), the decoder tables are staged as in the GEMV.
+// A workgroup of 4 waves takes 128 tokens and either two 64-row tiles (each
+// wave 32 rows by all 128 tokens, four 32-token MFMA groups: every decoded
+// block feeds twelve MFMAs) or one tile (each wave 32 rows by 64 tokens, two
+// groups), chosen per launch (gemm_kernel<TG>).  The activations of the 128
+// tokens go through LDS in chunks of 96 k (one group of four block columns),
+// the decoder tables are staged as in the GEMV.
 //
-// Work split: an item is a (64-row tile, 128-token group) pair and a unit is
+// Work split: an item is a (tile or tile pair, 128-token group) and a unit is
 // one chunk of an item (the trailing block columns of a row make one more,
-// shorter unit).  A fixed number of workgroups (two per CU) take equal
-// contiguous ranges of the items' units, so no launch leaves most of the
-// chip idle in a last partial wave of workgroups, however many tiles and
-// tokens there are.  An item whose units span several workgroups is combined
-// as in the GEMV: each publishes its sums through the per-device workspace
-// and the last to count in adds the pieces in workgroup order, which makes
-// the result independent of timing.
+// shorter unit).  A fixed number of workgroups (two per CU, fewer for few
+// items) take equal contiguous ranges of the items' units, so no launch
+// leaves most of the chip idle in a last partial wave of workgroups, however
+// many tiles and tokens there are.  An item whose units span several
+// workgroups is combined as in the GEMV: each publishes its sums through the
+// per-device workspace and the last to count in adds the pieces in workgroup
+// order, which makes the result independent of timing.
 #pragma once
 
 namespace tetra_dev {

@@ -600,7 +600,7 @@ def _encode_gpu(w, sigma, radii=None):
     """Words (uint64) of blocks w [n, 24] through tetra_encode."""
     n = w.shape[0]
     wd = torch.from_numpy(np.ascontiguousarray(w, dtype=np.float32)).cuda()
-    sd = torch.from_numpy(np.ascontiguousarray(np.broadcast_to(sigma, (n,)), dtype=np.float32)).cuda()
+    sd = torch.from_numpy(np.array(np.broadcast_to(sigma, (n,)), dtype=np.float32)).cuda()
     out = torch.zeros(3 * n, dtype=torch.int16, device="cuda")
     tt.encode(wd, sd, n, out, radii=radii)
     torch.cuda.synchronize()
