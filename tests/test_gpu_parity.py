@@ -561,6 +561,56 @@ def test_gemm_14b_shapes_sampled(name):
     _check_gemm(pk, workloads.activations(len(name), 203, K), rows=_sample_rows(M, rng, n=96), label=name)
 
 
+def test_gemm_long_prompt_sampled():
+    """2048 tokens on the 14B k shape (items cut into pieces over the whole
+    grid), every row of a sample checked for the first, middle and last
+    tokens."""
+    shapes = {n: (M, K) for n, M, K in workloads.layer_shapes("14B")}
+    M, K = shapes["k"]
+    N = 2048
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(3, 9), M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(2048, N, K)
+    y = torch.empty((N, M), dtype=torch.float32, device="cuda")
+    tt.gemm(pk.blob, pk.sigma, _f16_dev(x), y, M, K, N)
+    torch.cuda.synchronize()
+    toks = np.array([0, 1, 127, 128, 1023, 2046, 2047])
+    rows = _sample_rows(M, np.random.default_rng(12), n=48)
+    yr, norm = ogemv.gemv_f64(pk.words, pk.sigma_h, pk.tail, x[toks], rows=rows)
+    yg = y.cpu().numpy()[toks][:, rows].astype(np.float64)
+    worst = float((np.abs(yg - yr) / np.maximum(norm, 1e-300)).max())
+    print(f"[gemm long] M={M} K={K} N={N} worst={worst:.3e}", flush=True)
+    assert worst <= TOL_PAPER
+
+
+def test_gemm_token_slices():
+    """A prompt one token longer than a launch's slice (the largest multiple
+    of 128 tokens whose activations stay under 2 GiB: 61,568 tokens of
+    K = 17408) runs as two launches; tokens on both sides of the boundary,
+    the first and the last, against the oracle (activations drawn on the
+    device by a seeded generator, the sampled token rows copied back for the
+    oracle)."""
+    M, K = 64, 17408
+    slice_tokens = ((0x7FFFFFFF // (2 * K)) // 128) * 128
+    N = slice_tokens + 1
+    assert slice_tokens * K * 2 < 2 ** 31 <= (slice_tokens + 128) * K * 2
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(3, 11), M, K)
+    pk = Packed(words, sigma, tail, K)
+    gen = torch.Generator(device="cuda").manual_seed(0x7E7A_0090)
+    xd = torch.randn((N, K), generator=gen, device="cuda").half()
+    y = torch.empty((N, M), dtype=torch.float32, device="cuda")
+    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N)
+    torch.cuda.synchronize()
+    toks = np.array([0, 1, slice_tokens - 2, slice_tokens - 1, slice_tokens])
+    xs = xd[torch.as_tensor(toks, device="cuda")].cpu().numpy()
+    del xd
+    yr, norm = ogemv.gemv_f64(pk.words, pk.sigma_h, pk.tail, xs)
+    yg = y[torch.as_tensor(toks, device="cuda")].cpu().numpy().astype(np.float64)
+    worst = float((np.abs(yg - yr) / np.maximum(norm, 1e-300)).max())
+    print(f"[gemm slices] M={M} K={K} N={N} slice={slice_tokens} worst={worst:.3e}", flush=True)
+    assert worst <= TOL_PAPER
+
+
 @pytest.mark.parametrize("M,K,N", [(1024, 5120, 203), (200, 1536, 1), (4096, 2400, 129), (2100, 256, 77)])
 def test_gemm_split_items_repeat_bitwise(M, K, N):
     """Items cut across workgroups (16 pieces each for 1024 x 5120 at 203 tokens,
