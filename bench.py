@@ -259,15 +259,25 @@ def cpu_baseline(torch, tt, plan, seconds):
 
 
 KERNEL_SOURCES = ("paper_2609_35465_amd/csrc/kernels.h", "paper_2609_35465_amd/csrc/device_tables.h",
-                  "paper_2609_35465_amd/csrc/word_format.h", "paper_2609_35465_amd/csrc/tetra.hip")
+                  "paper_2609_35465_amd/csrc/word_format.h")
+LAUNCH_SOURCE = "paper_2609_35465_amd/csrc/tetra.hip"
 TRAFFIC_PROFILE = "profiles/gemv_kernel_qwen3-14b-40-layers_traffic.md"
 
 
 def kernel_source_hash():
+    """sha256 over what decides the measured kernel: the device sources of the
+    GEMV, its launch planning (the `launch_gemv` function of the library) and
+    the compiler flags."""
     import hashlib
+    from paper_2609_35465_amd import build as _build
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         h.update(open(os.path.join(ROOT, f), "rb").read())
+    lines = open(os.path.join(ROOT, LAUNCH_SOURCE), encoding="utf-8").read().split("\n")
+    start = next(i for i, l in enumerate(lines) if l.startswith("int launch_gemv("))
+    end = next(i for i in range(start, len(lines)) if lines[i] == "}")
+    h.update("\n".join(lines[start:end + 1]).encode())
+    h.update(" ".join(_build.HIP_FLAGS).encode())
     return h.hexdigest()
 
 

@@ -73,29 +73,30 @@ int ensure_tables(int* dev_out) {
     if (hipMemcpyToSymbol(HIP_SYMBOL(tetra_dev::g_packed), pk, sizeof(*pk), 0, hipMemcpyHostToDevice) !=
         hipSuccess)
         return TETRA_EDEVICE;
-    Workspace& ws = g_ws[dev];
-    ws.max_waves = num_cus(dev) * tetra_dev::kGemvGroupsPerCU * tetra_dev::kGemvWaves;
-    const int max_groups = ws.max_waves / tetra_dev::kGemvWaves;
+    // both workspaces, zeroed; on any failure nothing stays allocated and the
+    // next call tries again
+    const int max_waves = num_cus(dev) * tetra_dev::kGemvGroupsPerCU * tetra_dev::kGemvWaves;
+    const int max_groups = max_waves / tetra_dev::kGemvWaves;
     const size_t ws_bytes = tetra_dev::gemv_workspace_bytes(max_groups, TETRA_MAX_BATCH);
+    const int gemm_workers = num_cus(dev) * tetra_dev::kPfGroupsPerCU;
+    const size_t gemm_bytes = tetra_dev::gemm_workspace_bytes(gemm_workers);
     void* mem = nullptr;
-    if (hipMalloc(&mem, ws_bytes) != hipSuccess) return TETRA_EDEVICE;
-    if (hipMemset(mem, 0, ws_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
-        (void)hipFree(mem);
+    void* gmem = nullptr;
+    if (hipMalloc(&mem, ws_bytes) != hipSuccess || hipMalloc(&gmem, gemm_bytes) != hipSuccess ||
+        hipMemset(mem, 0, ws_bytes) != hipSuccess || hipMemset(gmem, 0, gemm_bytes) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+        if (mem) (void)hipFree(mem);
+        if (gmem) (void)hipFree(gmem);
         return TETRA_EDEVICE;
     }
+    Workspace& ws = g_ws[dev];
+    ws.max_waves = max_waves;
     ws.counters = static_cast<uint32_t*>(mem);
     ws.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(mem) + sizeof(uint32_t) * max_groups);
-    ws.gemm_workers = num_cus(dev) * tetra_dev::kPfGroupsPerCU;
-    const size_t gemm_bytes = tetra_dev::gemm_workspace_bytes(ws.gemm_workers);
-    void* gmem = nullptr;
-    if (hipMalloc(&gmem, gemm_bytes) != hipSuccess) return TETRA_EDEVICE;
-    if (hipMemset(gmem, 0, gemm_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
-        (void)hipFree(gmem);
-        return TETRA_EDEVICE;
-    }
+    ws.gemm_workers = gemm_workers;
     ws.gemm_counters = static_cast<uint32_t*>(gmem);
     ws.gemm_partials =
-        reinterpret_cast<float*>(static_cast<uint8_t*>(gmem) + sizeof(uint32_t) * static_cast<size_t>(ws.gemm_workers));
+        reinterpret_cast<float*>(static_cast<uint8_t*>(gmem) + sizeof(uint32_t) * static_cast<size_t>(gemm_workers));
     g_init_done[dev] = true;
     return TETRA_OK;
 }
