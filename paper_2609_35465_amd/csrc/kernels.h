@@ -387,6 +387,14 @@ __device__ __forceinline__ void finish_pending(Pipe<B>& st) {
 template <int B, bool Full>
 __device__ __forceinline__ void run_item(Pipe<B>& st, const ItemWords& cw, const ItemWords& nw, int col0,
                                          int ncol0, int kb, int ke, lds_bytes* L, const_u32* xc, int kp) {
+    // batch > 1: one activation pointer per row for the item, so that the
+    // block and word offsets go into the loads' immediate offsets instead of
+    // one 64-bit address per block and row (which spilled into lanes of VGPRs)
+    const_u32* xb[Pipe<B>::kStageX ? 1 : B];
+    if constexpr (!Pipe<B>::kStageX) {
+#pragma unroll
+        for (int bb = 0; bb < B; ++bb) xb[bb] = xc + (bb * kp + 12 * col0);
+    }
 #pragma unroll
     for (int k = 0; k < tetra::kGroupCols; ++k) {
         if (Full || (k >= kb && k < ke)) {
@@ -405,6 +413,18 @@ __device__ __forceinline__ void run_item(Pipe<B>& st, const ItemWords& cw, const
             nxt = fetch_block(lo, hi, L);
             uint32_t xn[Pipe<B>::kStageX ? B : 1][12];
             load_x<B>(xn, xc, kp, ncol);
+            // batch > 1: this block's activations, requested here so that the
+            // scalar loads (often scalar-cache misses: B rows of x pass
+            // through the cache) are in flight during the decode below; a
+            // second set, one block ahead as at batch 1, would not fit in the
+            // scalar registers
+            uint32_t xk[Pipe<B>::kStageX ? 1 : B][12];
+            if constexpr (!Pipe<B>::kStageX) {
+#pragma unroll
+                for (int bb = 0; bb < B; ++bb)
+#pragma unroll
+                    for (int q = 0; q < 12; ++q) xk[bb][q] = xb[bb][12 * k + q];
+            }
             __builtin_amdgcn_sched_barrier(0);
             // values and norm of the current block (its reads were waited for one block ago)
             uint32_t y[12];
@@ -421,7 +441,7 @@ __device__ __forceinline__ void run_item(Pipe<B>& st, const ItemWords& cw, const
                 for (int q = 0; q < 12; ++q) {
                     uint32_t xv;
                     if constexpr (Pipe<B>::kStageX) xv = st.x[bb][q];
-                    else xv = xc[bb * kp + 12 * (col0 + k) + q];
+                    else xv = xk[bb][q];
                     dt = dot2(y[q], xv, dt);
                 }
                 asm volatile("" : : "v"(dt));      // computed here, not sunk into the next block
