@@ -133,9 +133,13 @@ int tetra_unpack_rows(const void* codes, size_t codes_bytes, int M, int K,
 /*
  * Fused decode and matrix-vector product (Sec. 5.1, Eq. 2).  The blocks are
  * split evenly over the waves of the launch; pieces of a row tile held by
- * several waves are added in a fixed order, so y is deterministic and the
- * row for activation b of a batch-B call equals the batch-1 result for x_b
- * bit for bit (a grouped call may round differently from single calls):
+ * several waves are added in a fixed order, so y is deterministic.  The wave
+ * count follows the shapes, the device and how many workgroups of the
+ * batch's kernel a CU holds (on MI355X two for batch 1-2, one for 3-8); calls
+ * whose batch sizes fall in the same class split alike, so the row for
+ * activation b equals, bit for bit, the row of any other such call for x_b
+ * (small launches, with fewer waves than one round, split alike at every
+ * batch; a grouped call may round differently from single calls):
  *   y[b][row] = sigma_row * sum_blk s_blk * sum_j y_j x[b][24*blk + j]
  *               + sum_t tail[row][t] * x[b][24*nblk + t]
  * with s_blk = gain[g] * (1/sqrt(16 m)) in f32 and f32 accumulation.

@@ -13,7 +13,7 @@ constexpr int kTile = 64;                 // rows per code tile = lanes per wave
 constexpr int kChunk = kTile * 6;         // bytes per (tile, block column) chunk
 constexpr int kGemvWaves = 12;                 // waves per GEMV workgroup
 constexpr int kGemvThreads = kGemvWaves * 64;
-constexpr int kGemvGroupsPerCU = 2;            // at batch 1: 2 x 56.5 KB of LDS, 6 waves per SIMD
+constexpr int kGemvGroupsPerCU = 2;            // at most (batch 1: 2 x 56.5 KB of LDS, 6 waves per SIMD)
 constexpr int kMaxGroup = 16;
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
@@ -264,9 +264,10 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
 // pieces of a tile are combined in two levels (gemv_kernel): in LDS among
 // the waves of a workgroup, then through the per-device workspace among
 // workgroups, each time by the last to count in, in a fixed order.  The
-// ranges depend only on the shapes and W, never on timing or on the batch,
-// so the result is deterministic and row b of a batch-B product is the
-// batch-1 product of x_b bit for bit.
+// ranges depend only on the shapes and W, never on timing, so the result is
+// deterministic.  W depends on the batch only through the kernel's
+// residency (gemv_waves): row b of a batch-B product is bit for bit the row
+// of x_b at any batch size with the same residency.
 //
 // Inside its range a wave runs the blocks as a pipeline: the table reads and
 // activation loads of the next block are issued before the current block's
@@ -297,14 +298,16 @@ struct GemvGroup {
     int n, waves;
 };
 
-// wave count of a launch: two 768-thread workgroups per CU, fewer when the
-// launch is small, so that each wave takes at least kGemvMinBlocks blocks (a
-// wave's fixed cost, table staging and its share of the piece reduction, is
-// worth several blocks of streaming; every range is non-empty); independent
-// of the batch size
+// wave count of a launch: one round of the 768-thread workgroups a CU holds
+// at once (`groups`: two at batch 1 and 2; one from batch 3 on, whose
+// registers allow 12 waves per CU), fewer when the launch is small, so that
+// each wave takes at least kGemvMinBlocks blocks (a wave's fixed cost, table
+// staging and its share of the piece reduction, is worth several blocks of
+// streaming; every range is non-empty).  A second round of workgroups would
+// pay the launch start and the piece reduction twice.
 constexpr uint32_t kGemvMinBlocks = 8;
-inline int gemv_waves(uint32_t total, int cus) {
-    const uint32_t cap = static_cast<uint32_t>(cus) * kGemvGroupsPerCU * kGemvWaves;
+inline int gemv_waves(uint32_t total, int cus, int groups) {
+    const uint32_t cap = static_cast<uint32_t>(cus) * static_cast<uint32_t>(groups) * kGemvWaves;
     const uint32_t want = total / kGemvMinBlocks > 0 ? total / kGemvMinBlocks : 1u;
     return static_cast<int>(want < cap ? want : cap);
 }
@@ -632,6 +635,285 @@ __device__ __forceinline__ void run_piece(const GemvProblem& P, Piece& pc, lds_b
     for (int bb = 0; bb < B; ++bb) out[bb] = st.acc[bb];
 }
 
+// ------------------------------------------------ batch 3..8: matrix cores
+//
+// At batch B >= 3 the product of a block column is a small dense contraction
+// (64 rows x 24 weights by 24 x B activations), and it goes to the matrix
+// cores: v_mfma_f32_4x4x4f16 multiplies, in 16 blocks of four lanes, a 4 x 4
+// fp16 operand held one row per lane by a 4 x 4 operand held one column per
+// lane.  The A operand is the block's decoded values as the lane already
+// holds them (lane = row, coordinates 4c..4c+3 in y[2c], y[2c+1]), the B
+// operand four rows of x (lane 4i + j holds x_j), so six instructions give
+// the block's dot products for four batch rows; a second set of six covers
+// rows 4..7.  The result sits in lane 4i + j, register r: row 4i + r, batch
+// row j.  Each row's block scale comes to the four lanes of its quad by a
+// DPP quad broadcast, so the sums take four fused multiply-adds per block
+// and set, where the VALU dot product took 12 per batch row.  Batches 1 and
+// 2 keep the VALU dot product of run_item: at batch 2 its registers leave
+// room for two workgroups per CU, which this path's do not (measured: the
+// VALU path is 3 % faster there, this one 9 % at batch 3, 16 % at 4 and 37 %
+// at 8).
+//
+// The activations of a group of four block columns pass through a 1 KB LDS
+// slot per wave and set: one 16-byte load per lane, requested a group ahead
+// together with the group's code words (so that waiting for it never waits
+// for later code words), written at the group's start, and read back per
+// block as three broadcast ds_read_b128 per lane (four distinct addresses
+// per wave, 48 bytes apart: no bank conflict).  Every output column is
+// computed by the same instructions whatever the other columns hold, so row
+// b of a batch-B product (3 <= B <= 8) is the same bit for bit at every such
+// B.
+
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+
+constexpr int kXSlotBytes = 1024;      // per wave and set of four batch rows: 768 B of x, or the 4 x 64 sums
+constexpr int kXBlockBytes = 192;      // one block column of four rows of x (4 x 48 B)
+
+template <int B>
+struct MxSets {
+    static constexpr int kN = (B + 3) / 4;
+};
+
+// one group's activations for every set of four batch rows, one 16-byte
+// segment per lane: segment m = lane mod 48 is part m mod 3 of block
+// column (m mod 12) / 3 of row m / 12 of the set
+template <int B>
+struct XGroup {
+    u32x4 v[MxSets<B>::kN];
+};
+
+template <int B>
+struct XPiece {
+    XGroup<B> g;        // the piece's first group (the trailing columns when it starts there)
+};
+
+struct XSeg {
+    int r, k, part;
+};
+
+__device__ __forceinline__ XSeg x_segment() {
+    const int l = lane_now();
+    const int m = l >= 48 ? l - 48 : l;
+    XSeg s;
+    s.r = m / 12;
+    s.k = (m - 12 * s.r) / 3;
+    s.part = m - 12 * s.r - 3 * s.k;
+    return s;
+}
+
+// activations of block columns 4j..4j+3 (clamped to the last block column;
+// rows past the batch read the last row: their products are never used)
+template <int B>
+__device__ __forceinline__ XGroup<B> load_xgroup(const GemvProblem& P, int j) {
+    const XSeg sg = x_segment();
+    const int col = min(4 * j + sg.k, P.nblk - 1);
+    const uint8_t* xb = reinterpret_cast<const uint8_t*>(P.x) + 48 * col + 16 * sg.part;
+    XGroup<B> g;
+#pragma unroll
+    for (int s = 0; s < MxSets<B>::kN; ++s) {
+        const int row = min(4 * s + sg.r, B - 1);
+        g.v[s] = *reinterpret_cast<const u32x4_a4*>(xb + static_cast<size_t>(row) * P.K * 2);
+    }
+    return g;
+}
+
+// the activation load of a piece's first group, unconditional: a wave with
+// no piece (live false) reads group 0
+template <int B>
+__device__ __forceinline__ XPiece<B> begin_xpiece(const GemvProblem& P, const Piece& pc, bool live) {
+    XPiece<B> xp;
+    xp.g = load_xgroup<B>(P, live ? pc.j : 0);
+    return xp;
+}
+
+// xs: the wave's slots
+template <int B>
+__device__ __forceinline__ void write_xgroup(uint8_t* xs, const XGroup<B>& g) {
+    const XSeg sg = x_segment();
+    const int off = sg.k * kXBlockBytes + sg.r * 48 + sg.part * 16;
+#pragma unroll
+    for (int s = 0; s < MxSets<B>::kN; ++s) *reinterpret_cast<u32x4*>(xs + s * kXSlotBytes + off) = g.v[s];
+}
+
+__device__ __forceinline__ half4_t as_half4(uint32_t a, uint32_t b) {
+    const u32x2 v = {a, b};
+    return __builtin_bit_cast(half4_t, v);
+}
+
+template <int I>
+__device__ __forceinline__ float quad_bcast(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x55 * I, 0xF, 0xF, false));
+}
+
+template <int B>
+struct MxPipe {
+    BlockFetch cur;
+    float ps;                          // scale of the previous block (zero before the first)
+    f32x4 d[MxSets<B>::kN];            // products of the previous block
+    f32x4 acc[MxSets<B>::kN];
+};
+
+template <int B>
+__device__ __forceinline__ void mx_finish(MxPipe<B>& st) {
+    const float p0 = quad_bcast<0>(st.ps), p1 = quad_bcast<1>(st.ps);
+    const float p2 = quad_bcast<2>(st.ps), p3 = quad_bcast<3>(st.ps);
+#pragma unroll
+    for (int s = 0; s < MxSets<B>::kN; ++s) {
+        st.acc[s].x = fmaf(p0, st.d[s].x, st.acc[s].x);
+        st.acc[s].y = fmaf(p1, st.d[s].y, st.acc[s].y);
+        st.acc[s].z = fmaf(p2, st.d[s].z, st.acc[s].z);
+        st.acc[s].w = fmaf(p3, st.d[s].w, st.acc[s].w);
+    }
+}
+
+// six products of a block for one set: y (A, this lane's row) by the three
+// 16-byte reads of x (B)
+__device__ __forceinline__ f32x4 mx_block(const uint32_t (&y)[12], u32x4 x0, u32x4 x1, u32x4 x2) {
+    const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    f32x4 d = __builtin_amdgcn_mfma_f32_4x4x4f16(as_half4(y[0], y[1]), as_half4(x0.x, x0.y), z, 0, 0, 0);
+    d = __builtin_amdgcn_mfma_f32_4x4x4f16(as_half4(y[2], y[3]), as_half4(x0.z, x0.w), d, 0, 0, 0);
+    d = __builtin_amdgcn_mfma_f32_4x4x4f16(as_half4(y[4], y[5]), as_half4(x1.x, x1.y), d, 0, 0, 0);
+    d = __builtin_amdgcn_mfma_f32_4x4x4f16(as_half4(y[6], y[7]), as_half4(x1.z, x1.w), d, 0, 0, 0);
+    d = __builtin_amdgcn_mfma_f32_4x4x4f16(as_half4(y[8], y[9]), as_half4(x2.x, x2.y), d, 0, 0, 0);
+    d = __builtin_amdgcn_mfma_f32_4x4x4f16(as_half4(y[10], y[11]), as_half4(x2.z, x2.w), d, 0, 0, 0);
+    return d;
+}
+
+// Blocks kb..ke-1 of one item, as run_item; xr: the wave's slots plus 48
+// times the lane's batch row within a set (lane mod 4)
+template <int B, bool Full>
+__device__ __forceinline__ void run_item_mx(MxPipe<B>& st, const ItemWords& cw, const ItemWords& nw, int kb, int ke,
+                                            lds_bytes* L, const uint8_t* xr) {
+    constexpr int NS = MxSets<B>::kN;
+#pragma unroll
+    for (int k = 0; k < tetra::kGroupCols; ++k) {
+        if (Full || (k >= kb && k < ke)) {
+            uint32_t lo, hi;
+            if (k + 1 < tetra::kGroupCols && (Full || k + 1 < ke)) {
+                if (k == 0) block_word<1>(cw, lo, hi);
+                else if (k == 1) block_word<2>(cw, lo, hi);
+                else block_word<3>(cw, lo, hi);
+            } else {
+                block_word<0>(nw, lo, hi);
+            }
+            const BlockFetch nxt = fetch_block(lo, hi, L);
+            u32x4 xv[NS][3];
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+#pragma unroll
+                for (int c = 0; c < 3; ++c)
+                    xv[s][c] = *reinterpret_cast<const u32x4*>(xr + s * kXSlotBytes + k * kXBlockBytes + 16 * c);
+            __builtin_amdgcn_sched_barrier(0);
+            uint32_t y[12];
+            const uint32_t sa = block_values(st.cur, y);
+            __builtin_amdgcn_sched_barrier(0);
+            // one wait per block: the next block's table reads, this block's
+            // activations and the previous block's scale
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            mx_finish<B>(st);
+            st.ps = *(lds_f32*)(L + kScaleOff + sa);
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                st.d[s] = mx_block(y, xv[s][0], xv[s][1], xv[s][2]);
+                asm volatile("" : : "v"(st.d[s]));     // computed here, not sunk into the next block
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            st.cur = nxt;
+        }
+    }
+}
+
+template <int B>
+__device__ __forceinline__ void run_one_item_mx(MxPipe<B>& st, int kb, int ke, const ItemWords& cw,
+                                                const ItemWords& nw, lds_bytes* L, const uint8_t* xr) {
+    if (kb == 0 && ke == tetra::kGroupCols)
+        run_item_mx<B, true>(st, cw, nw, 0, tetra::kGroupCols, L, xr);
+    else
+        run_item_mx<B, false>(st, cw, nw, kb, ke, L, xr);
+}
+
+template <int B>
+__device__ __forceinline__ void start_pipe_mx(MxPipe<B>& st, const ItemWords& w, int kb, lds_bytes* L) {
+    uint32_t lo, hi;
+    if (kb == 0) block_word<0>(w, lo, hi);
+    else if (kb == 1) block_word<1>(w, lo, hi);
+    else if (kb == 2) block_word<2>(w, lo, hi);
+    else block_word<3>(w, lo, hi);
+    st.cur = fetch_block(lo, hi, L);
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    st.ps = 0.f;
+#pragma unroll
+    for (int s = 0; s < MxSets<B>::kN; ++s) st.d[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// run_piece for 3 <= B <= 8.  xs: the wave's LDS slots (kXSlotBytes per
+// set); the piece's sums come back one row per lane through the same slots.
+template <int B>
+__device__ __forceinline__ void run_piece_mx(const GemvProblem& P, Piece& pc, const XPiece<B>& xp, lds_bytes* L,
+                                             uint8_t* xs, float (&out)[B]) {
+    constexpr int NS = MxSets<B>::kN;
+    const int lane = threadIdx.x & 63;
+    const uint8_t* tb = P.codes + static_cast<size_t>(pc.t) * P.nblk * kChunk;
+    const uint8_t* xr = xs + 48 * (threadIdx.x & 3);
+    const int jg = pc.jg;
+    int j = pc.j;
+    int kb = pc.c0 - 4 * j;
+    MxPipe<B> st;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) st.acc[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // x of group j + 1 is requested at the start of group j; after the last
+    // group that is the trailing columns' group (ng), when the piece has them
+    const int jx = pc.tr ? P.ng : jg;
+    XGroup<B> xn = xp.g;
+    if (j <= jg) {
+        const int kl = __builtin_amdgcn_readfirstlane(pc.tr ? tetra::kGroupCols : pc.c1 - 4 * jg);
+        write_xgroup<B>(xs, xn);
+        xn = load_xgroup<B>(P, min(j + 1, jx));
+        start_pipe_mx<B>(st, pc.cw, kb, L);
+        ItemWords wa = pc.cw, wb = pc.nw;
+        for (;;) {
+            run_one_item_mx<B>(st, kb, j == jg ? kl : tetra::kGroupCols, wa, wb, L, xr);
+            if (j == jg) break;
+            ++j;
+            kb = 0;
+            write_xgroup<B>(xs, xn);
+            wa = load_group(tb, min(j + 1, jg), lane);
+            xn = load_xgroup<B>(P, min(j + 1, jx));
+            run_one_item_mx<B>(st, 0, j == jg ? kl : tetra::kGroupCols, wb, wa, L, xr);
+            if (j == jg) break;
+            ++j;
+            write_xgroup<B>(xs, xn);
+            wb = load_group(tb, min(j + 1, jg), lane);
+            xn = load_xgroup<B>(P, min(j + 1, jx));
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        mx_finish<B>(st);
+        kb = 0;
+    }
+    if (pc.tr) {
+        const int c = 4 * P.ng;
+        ItemWords tw = pc.tw;
+        trailing_fixup(tw, P.rem);
+        write_xgroup<B>(xs, xn);
+        start_pipe_mx<B>(st, tw, kb, L);
+        run_item_mx<B, false>(st, tw, tw, kb, pc.c1 - c, L, xr);
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        mx_finish<B>(st);
+    }
+    // lane 4i + j holds rows 4i..4i+3 of batch row 4s + j: through the slots
+    // (after the last reads of x, LDS operations of a wave being in order)
+    // to one row per lane
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+        *reinterpret_cast<f32x4*>(xs + s * kXSlotBytes + 256 * (threadIdx.x & 3) + 16 * ((threadIdx.x & 63) >> 2)) =
+            st.acc[s];
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) out[bb] = *reinterpret_cast<const float*>(xs + 256 * bb + 4 * (threadIdx.x & 63));
+}
+
 // y of a tile's rows: sigma_row * sum + unquantised tail (T = K mod 24 is
 // even, so the tail is at most 11 fp16 pairs).  load_rows issues the loads,
 // store_rows does the arithmetic and the stores, so that the loads can be in
@@ -674,11 +956,13 @@ __device__ __forceinline__ void store_rows(const GemvProblem& P, int t, const fl
 // workgroup's sum goes to the workspace, where the last workgroup to arrive
 // adds them in workgroup order.
 template <int B>
-__global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(B == 1 ? 6 : B <= 4 ? 4 : 2)))
+__global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(B <= 2 ? 6 : 3)))
 void gemv_kernel(const GemvGroup grp) {
     __shared__ uint4 s_tab[kPackedTableBytes / 16];
     __shared__ float s_piece[kGemvWaves * 2 * B * 64];   // [wave][first/last piece][B][64]
     __shared__ uint32_t s_cnt[2 * kGemvWaves];
+    constexpr bool kMx = B >= 3;
+    __shared__ uint4 s_xs[kMx ? kGemvWaves * MxSets<B>::kN * kXSlotBytes / 16 : 1];   // batch >= 3: x slots per wave
     if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
     lds_bytes* L = (lds_bytes*)(s_tab);
     const int lane = threadIdx.x & 63;
@@ -705,6 +989,9 @@ void gemv_kernel(const GemvGroup grp) {
     // the first piece's code words are requested while the tables arrive;
     // the barrier orders LDS only, so they stay in flight across it
     Piece pc = begin_piece_live(grp.prob[p], t, c, c1, lane, w < W);
+    XPiece<B> xp;
+    if constexpr (kMx) xp = begin_xpiece<B>(grp.prob[p], pc, w < W);
+    uint8_t* xs = reinterpret_cast<uint8_t*>(s_xs) + (kMx ? wid * MxSets<B>::kN * kXSlotBytes : 0);
     ts.store(s_tab);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
     __builtin_amdgcn_s_barrier();
@@ -714,7 +1001,8 @@ void gemv_kernel(const GemvGroup grp) {
     for (;;) {
         const GemvProblem& P = grp.prob[p];
         float sum[B];
-        run_piece<B>(P, pc, L, sum);
+        if constexpr (kMx) run_piece_mx<B>(P, pc, xp, L, xs, sum);
+        else run_piece<B>(P, pc, L, sum);
         if (c == 0 && c1 == P.nblk) {
             const RowTail rt = load_rows(P, t);
             store_rows<B>(P, t, sum, rt);
@@ -813,6 +1101,7 @@ void gemv_kernel(const GemvGroup grp) {
         const uint32_t left = end - i;
         c1 = left < static_cast<uint32_t>(grp.prob[p].nblk) ? static_cast<int>(left) : grp.prob[p].nblk;
         pc = begin_piece(grp.prob[p], t, 0, c1, lane);
+        if constexpr (kMx) xp = begin_xpiece<B>(grp.prob[p], pc, true);
     }
 }
 

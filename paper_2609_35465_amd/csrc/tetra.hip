@@ -40,6 +40,7 @@ struct Workspace {
     uint32_t* gemm_counters = nullptr;
     float* gemm_partials = nullptr;
     int gemm_workers = 0;
+    int gemv_groups[TETRA_MAX_BATCH + 1] = {};    // resident GEMV workgroups per CU, by batch
 };
 Workspace g_ws[kMaxDevices];
 
@@ -48,6 +49,17 @@ int num_cus(int dev) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
         return 256;
     return n;
+}
+
+// workgroups of gemv_kernel<B> one CU holds at once (registers and LDS of
+// the compiled kernel), between 1 and kGemvGroupsPerCU; 0 on an error
+template <int B>
+int gemv_resident() {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(&tetra_dev::gemv_kernel<B>),
+                                                     tetra_dev::kGemvThreads, 0) != hipSuccess)
+        return 0;
+    return std::max(1, std::min(n, tetra_dev::kGemvGroupsPerCU));
 }
 
 int ensure_tables(int* dev_out) {
@@ -73,6 +85,12 @@ int ensure_tables(int* dev_out) {
     if (hipMemcpyToSymbol(HIP_SYMBOL(tetra_dev::g_packed), pk, sizeof(*pk), 0, hipMemcpyHostToDevice) !=
         hipSuccess)
         return TETRA_EDEVICE;
+    static_assert(TETRA_MAX_BATCH == 8, "one residency entry per batch size");
+    const int resident[TETRA_MAX_BATCH + 1] = {0, gemv_resident<1>(), gemv_resident<2>(), gemv_resident<3>(),
+                                               gemv_resident<4>(), gemv_resident<5>(), gemv_resident<6>(),
+                                               gemv_resident<7>(), gemv_resident<8>()};
+    for (int b = 1; b <= TETRA_MAX_BATCH; ++b)
+        if (resident[b] == 0) return TETRA_EDEVICE;
     // both workspaces, zeroed; on any failure nothing stays allocated and the
     // next call tries again
     const int max_waves = num_cus(dev) * tetra_dev::kGemvGroupsPerCU * tetra_dev::kGemvWaves;
@@ -91,6 +109,7 @@ int ensure_tables(int* dev_out) {
     }
     Workspace& ws = g_ws[dev];
     ws.max_waves = max_waves;
+    for (int b = 0; b <= TETRA_MAX_BATCH; ++b) ws.gemv_groups[b] = resident[b];
     ws.counters = static_cast<uint32_t*>(mem);
     ws.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(mem) + sizeof(uint32_t) * max_groups);
     ws.gemm_workers = gemm_workers;
@@ -155,7 +174,7 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t s
     const Workspace& ws = g_ws[dev];
     grp.n = n;
     grp.total = static_cast<uint32_t>(total);
-    grp.waves = std::min(tetra_dev::gemv_waves(grp.total, num_cus(dev)), ws.max_waves);
+    grp.waves = std::min(tetra_dev::gemv_waves(grp.total, num_cus(dev), ws.gemv_groups[batch]), ws.max_waves);
     grp.inv_total = 1.0 / static_cast<double>(grp.total);
     grp.inv_waves = 1.0 / static_cast<double>(grp.waves);
     grp.counters = ws.counters;

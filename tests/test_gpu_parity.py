@@ -146,10 +146,38 @@ def test_gemv_batches(batch):
     pk = Packed(words, sigma, tail, K)
     x = workloads.activations(500 + batch, batch, K)
     yb = _check_gemv(pk, x, label="batch")
-    # each batch row equals the batch-1 result for the same vector
+    # a launch this small has fewer waves than one round of workgroups at
+    # every batch, so it splits alike; batches 1-2 take the VALU dot product
+    # and 3-8 the matrix cores, so each row equals, bit for bit, the row of
+    # the same activation in a call of the smallest batch of its class
     for b in range(batch):
-        y1 = pk.gemv(x[b:b + 1])
-        assert np.array_equal(y1[0], yb[b])
+        if batch <= 2:
+            ref = pk.gemv(x[b:b + 1])[0]
+        else:
+            ref = pk.gemv(np.repeat(x[b:b + 1], 3, axis=0))[1]
+        assert np.array_equal(ref, yb[b])
+
+
+def test_gemv_batch_classes_on_a_full_launch():
+    """27,264 blocks: the wave count is one round of resident workgroups,
+    which on MI355X differs between batch 1-2 (VALU dot product, two
+    workgroups per CU) and batch 3-8 (matrix cores, one).  Within a class a
+    row is bit for bit the row of the same activation at another batch;
+    every batch is within the parity bound of the oracle."""
+    M, K = 8192, 24 * 213 + 8
+    words, sigma, tail = workloads.tetra_matrix(77, M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(77, 8, K)
+    y = {b: pk.gemv(x[:b]) for b in (1, 2, 3, 4, 8)}
+    assert np.array_equal(y[2][0], y[1][0])
+    for b in (4, 8):
+        assert np.array_equal(y[b][:3], y[3])
+    rows = _sample_rows(M, np.random.default_rng(77))
+    yr, norm = ogemv.gemv_f64(words, sigma, tail, x, rows=rows)
+    for b, yb in y.items():
+        worst = float((np.abs(yb[:, rows].astype(np.float64) - yr[:b]) / np.maximum(norm[:b], 1e-300)).max())
+        print(f"[batch classes] batch={b} worst={worst:.3e}", flush=True)
+        assert worst <= TOL_PAPER
 
 
 def test_gemv_degenerate_inputs():
