@@ -139,6 +139,39 @@ def test_gemv_small_shapes(M, K):
     _check_gemv(pk, x, label="small")
 
 
+@pytest.mark.parametrize("batch", [3, 6])
+@pytest.mark.parametrize("M,K", SMALL_SHAPES)
+def test_gemv_small_shapes_matrix_cores(M, K, batch):
+    """The same shapes on the matrix-core path: one set of four batch rows
+    (batch 3) and two (batch 6), ragged row tiles, trailing block columns,
+    K tails and K = 24 (a tile with no whole group of four columns)."""
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(0, 3) + M + K, M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(M + K + batch, batch, K)
+    _check_gemv(pk, x, label=f"small b{batch}")
+
+
+@pytest.mark.parametrize("batch", [2, 3, 4, 5, 8])
+def test_gemv_one_hot_rows_pick_weight_columns(batch):
+    """Batch row b holds a single 1 at column k_b: row b of the product is
+    column k_b of the dequantised matrix.  The columns lie in the first and
+    second group of four blocks, the trailing block and the unquantised
+    tail, so a batch row's activations reaching another row's output, or a
+    shifted column, fails.  All-zero activations give exact zeros."""
+    M, K = 70, 24 * 9 + 8
+    words, sigma, tail = workloads.tetra_matrix(19, M, K)
+    pk = Packed(words, sigma, tail, K)
+    W = ogemv.dequant(words, sigma, tail)
+    cols = [0, 191, 23, 215, 96, 216, 24, 223][:batch]
+    x = np.zeros((batch, K), np.float16)
+    for b, k in enumerate(cols):
+        x[b, k] = 1.0
+    y = pk.gemv(x)
+    for b, k in enumerate(cols):
+        assert np.allclose(y[b], W[:, k], rtol=1e-6, atol=0), (b, k)
+    assert not pk.gemv(np.zeros((batch, K), np.float16)).any()
+
+
 @pytest.mark.parametrize("batch", list(range(1, 9)))
 def test_gemv_batches(batch):
     M, K = 192, 24 * 40 + 16
