@@ -135,11 +135,11 @@ int tetra_unpack_rows(const void* codes, size_t codes_bytes, int M, int K,
  * split evenly over the waves of the launch; pieces of a row tile held by
  * several waves are added in a fixed order, so y is deterministic.  The wave
  * count follows the shapes, the device and how many workgroups of the
- * batch's kernel a CU holds (on MI355X two for batch 1-2, one for 3-8); calls
- * whose batch sizes fall in the same class split alike, so the row for
- * activation b equals, bit for bit, the row of any other such call for x_b
- * (small launches, with fewer waves than one round, split alike at every
- * batch; a grouped call may round differently from single calls):
+ * batch's kernel a CU holds (on MI355X two for batch 1-2, one for 3-8).
+ * Batches 1-2 form the per-block sums with VALU dot products, batches 3-8
+ * on the matrix cores, which round differently; within each class the row
+ * for activation b equals, bit for bit, the row of any other call of the
+ * class for x_b (a grouped call may round differently from single calls):
  *   y[b][row] = sigma_row * sum_blk s_blk * sum_j y_j x[b][24*blk + j]
  *               + sum_t tail[row][t] * x[b][24*nblk + t]
  * with s_blk = gain[g] * (1/sqrt(16 m)) in f32 and f32 accumulation.
