@@ -650,9 +650,9 @@ __device__ __forceinline__ void run_piece(const GemvProblem& P, Piece& pc, lds_b
 // DPP quad broadcast, so the sums take four fused multiply-adds per block
 // and set, where the VALU dot product took 12 per batch row.  Batches 1 and
 // 2 keep the VALU dot product of run_item: at batch 2 its registers leave
-// room for two workgroups per CU, which this path's do not (measured: the
-// VALU path is 3 % faster there, this one 9 % at batch 3, 16 % at 4 and 37 %
-// at 8).
+// room for two workgroups per CU, which this path's do not (measured on a
+// 14B decode step: the VALU path is 3 % faster at batch 2, this one 9 % at
+// batch 3, 16 % at 4 and 48 % at 8).
 //
 // The activations of a group of four block columns pass through a 1 KB LDS
 // slot per wave and set: one 16-byte load per lane, requested a group ahead
@@ -685,11 +685,6 @@ struct XGroup {
     u32x4 v[MxSets<B>::kN];
 };
 
-template <int B>
-struct XPiece {
-    XGroup<B> g;        // the piece's first group (the trailing columns when it starts there)
-};
-
 struct XSeg {
     int r, k, part;
 };
@@ -720,13 +715,12 @@ __device__ __forceinline__ XGroup<B> load_xgroup(const GemvProblem& P, int j) {
     return g;
 }
 
-// the activation load of a piece's first group, unconditional: a wave with
-// no piece (live false) reads group 0
+// the activation load of a piece's first group (its trailing columns when
+// it starts there), unconditional: a wave with no piece (live false) reads
+// group 0
 template <int B>
-__device__ __forceinline__ XPiece<B> begin_xpiece(const GemvProblem& P, const Piece& pc, bool live) {
-    XPiece<B> xp;
-    xp.g = load_xgroup<B>(P, live ? pc.j : 0);
-    return xp;
+__device__ __forceinline__ XGroup<B> begin_xpiece(const GemvProblem& P, const Piece& pc, bool live) {
+    return load_xgroup<B>(P, live ? pc.j : 0);
 }
 
 // xs: the wave's slots
@@ -852,7 +846,7 @@ __device__ __forceinline__ void start_pipe_mx(MxPipe<B>& st, const ItemWords& w,
 // run_piece for 3 <= B <= 8.  xs: the wave's LDS slots (kXSlotBytes per
 // set); the piece's sums come back one row per lane through the same slots.
 template <int B>
-__device__ __forceinline__ void run_piece_mx(const GemvProblem& P, Piece& pc, const XPiece<B>& xp, lds_bytes* L,
+__device__ __forceinline__ void run_piece_mx(const GemvProblem& P, Piece& pc, const XGroup<B>& xp, lds_bytes* L,
                                              uint8_t* xs, float (&out)[B]) {
     constexpr int NS = MxSets<B>::kN;
     const int lane = threadIdx.x & 63;
@@ -867,7 +861,7 @@ __device__ __forceinline__ void run_piece_mx(const GemvProblem& P, Piece& pc, co
     // x of group j + 1 is requested at the start of group j; after the last
     // group that is the trailing columns' group (ng), when the piece has them
     const int jx = pc.tr ? P.ng : jg;
-    XGroup<B> xn = xp.g;
+    XGroup<B> xn = xp;
     if (j <= jg) {
         const int kl = __builtin_amdgcn_readfirstlane(pc.tr ? tetra::kGroupCols : pc.c1 - 4 * jg);
         write_xgroup<B>(xs, xn);
@@ -989,7 +983,7 @@ void gemv_kernel(const GemvGroup grp) {
     // the first piece's code words are requested while the tables arrive;
     // the barrier orders LDS only, so they stay in flight across it
     Piece pc = begin_piece_live(grp.prob[p], t, c, c1, lane, w < W);
-    XPiece<B> xp;
+    XGroup<B> xp;
     if constexpr (kMx) xp = begin_xpiece<B>(grp.prob[p], pc, w < W);
     uint8_t* xs = reinterpret_cast<uint8_t*>(s_xs) + (kMx ? wid * MxSets<B>::kN * kXSlotBytes : 0);
     ts.store(s_tab);
