@@ -151,6 +151,26 @@ def test_gemv_small_shapes_matrix_cores(M, K, batch):
     _check_gemv(pk, x, label=f"small b{batch}")
 
 
+def _random_gemv_cases(n=24, seed=2024):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        M = int(rng.integers(1, 300))
+        K = 24 * int(rng.integers(1, 41)) + 2 * int(rng.integers(0, 12))
+        cases.append((M, K, 1 + i % 8, int(rng.integers(1 << 30))))
+    return cases
+
+
+@pytest.mark.parametrize("M,K,batch,seed", _random_gemv_cases())
+def test_gemv_random_shapes_every_batch(M, K, batch, seed):
+    """Seeded random shapes (M 1-299, 1-40 blocks per row, any even tail)
+    at every batch size 1-8, both product paths, against the oracle."""
+    words, sigma, tail = workloads.tetra_matrix(seed, M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(seed + 1, batch, K)
+    _check_gemv(pk, x, label=f"random b{batch}")
+
+
 @pytest.mark.parametrize("batch", [2, 3, 4, 5, 8])
 def test_gemv_one_hot_rows_pick_weight_columns(batch):
     """Batch row b holds a single 1 at column k_b: row b of the product is
