@@ -655,11 +655,12 @@ __device__ __forceinline__ void run_piece(const GemvProblem& P, Piece& pc, lds_b
 // batch 3, 16 % at 4 and 48 % at 8).
 //
 // The activations of a group of four block columns pass through a 1 KB LDS
-// slot per wave and set: one 16-byte load per lane, requested a group ahead
+// slot per wave and set (MxSets::kRow bytes per block column and batch row,
+// 48 of them used): one 16-byte load per lane, requested a group ahead
 // together with the group's code words (so that waiting for it never waits
 // for later code words), written at the group's start, and read back per
 // block as three broadcast ds_read_b128 per lane (four distinct addresses
-// per wave, 48 bytes apart: no bank conflict).  Every output column is
+// per wave, 48 or 64 bytes apart: no bank conflict).  Every output column is
 // computed by the same instructions whatever the other columns hold, so row
 // b of a batch-B product (3 <= B <= 8) is the same bit for bit at every such
 // B.
@@ -669,17 +670,21 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
 
-constexpr int kXSlotBytes = 1024;      // per wave and set of four batch rows: 768 B of x, or the 4 x 64 sums
-constexpr int kXBlockBytes = 192;      // one block column of four rows of x (4 x 48 B)
+constexpr int kXSlotBytes = 1024;      // per wave and set of four batch rows: x of four block columns, or the 4 x 64 sums
 
+// kRow: bytes per block column and batch row in a slot.  With one set (batch
+// 3-4) a row takes 64 bytes, so that a lane's segment follows from its index
+// by shifts; with two sets (batch 5-8) rows are packed at 48 bytes (measured
+// 6 % faster at batch 8, where the registers are at their limit).
 template <int B>
 struct MxSets {
     static constexpr int kN = (B + 3) / 4;
+    static constexpr int kRow = kN == 1 ? 64 : 48;
+    static constexpr int kBlock = 4 * kRow;
 };
 
 // one group's activations for every set of four batch rows, one 16-byte
-// segment per lane: segment m = lane mod 48 is part m mod 3 of block
-// column (m mod 12) / 3 of row m / 12 of the set
+// segment per lane (x_segment)
 template <int B>
 struct XGroup {
     u32x4 v[MxSets<B>::kN];
@@ -689,13 +694,24 @@ struct XSeg {
     int r, k, part;
 };
 
+// 64-byte rows: lane l holds part l & 3 of block column (l >> 2) & 3 of
+// row l >> 4 (part 3 repeats part 2: a block row is 48 bytes).  48-byte rows:
+// segment m = l mod 48 is part m mod 3 of block column (m mod 12) / 3 of row
+// m / 12 (lanes 48-63 repeat lanes 0-15).
+template <int B>
 __device__ __forceinline__ XSeg x_segment() {
     const int l = lane_now();
-    const int m = l >= 48 ? l - 48 : l;
     XSeg s;
-    s.r = m / 12;
-    s.k = (m - 12 * s.r) / 3;
-    s.part = m - 12 * s.r - 3 * s.k;
+    if constexpr (MxSets<B>::kRow == 64) {
+        s.r = l >> 4;
+        s.k = (l >> 2) & 3;
+        s.part = l & 3;
+    } else {
+        const int m = l >= 48 ? l - 48 : l;
+        s.r = m / 12;
+        s.k = (m - 12 * s.r) / 3;
+        s.part = m - 12 * s.r - 3 * s.k;
+    }
     return s;
 }
 
@@ -703,9 +719,9 @@ __device__ __forceinline__ XSeg x_segment() {
 // rows past the batch read the last row: their products are never used)
 template <int B>
 __device__ __forceinline__ XGroup<B> load_xgroup(const GemvProblem& P, int j) {
-    const XSeg sg = x_segment();
+    const XSeg sg = x_segment<B>();
     const int col = min(4 * j + sg.k, P.nblk - 1);
-    const uint8_t* xb = reinterpret_cast<const uint8_t*>(P.x) + 48 * col + 16 * sg.part;
+    const uint8_t* xb = reinterpret_cast<const uint8_t*>(P.x) + 48 * col + 16 * min(sg.part, 2);
     XGroup<B> g;
 #pragma unroll
     for (int s = 0; s < MxSets<B>::kN; ++s) {
@@ -726,8 +742,8 @@ __device__ __forceinline__ XGroup<B> begin_xpiece(const GemvProblem& P, const Pi
 // xs: the wave's slots
 template <int B>
 __device__ __forceinline__ void write_xgroup(uint8_t* xs, const XGroup<B>& g) {
-    const XSeg sg = x_segment();
-    const int off = sg.k * kXBlockBytes + sg.r * 48 + sg.part * 16;
+    const XSeg sg = x_segment<B>();
+    const int off = sg.k * MxSets<B>::kBlock + sg.r * MxSets<B>::kRow + sg.part * 16;
 #pragma unroll
     for (int s = 0; s < MxSets<B>::kN; ++s) *reinterpret_cast<u32x4*>(xs + s * kXSlotBytes + off) = g.v[s];
 }
@@ -776,7 +792,7 @@ __device__ __forceinline__ f32x4 mx_block(const uint32_t (&y)[12], u32x4 x0, u32
     return d;
 }
 
-// Blocks kb..ke-1 of one item, as run_item; xr: the wave's slots plus 48
+// Blocks kb..ke-1 of one item, as run_item; xr: the wave's slots plus kRow
 // times the lane's batch row within a set (lane mod 4)
 template <int B, bool Full>
 __device__ __forceinline__ void run_item_mx(MxPipe<B>& st, const ItemWords& cw, const ItemWords& nw, int kb, int ke,
@@ -799,7 +815,7 @@ __device__ __forceinline__ void run_item_mx(MxPipe<B>& st, const ItemWords& cw, 
             for (int s = 0; s < NS; ++s)
 #pragma unroll
                 for (int c = 0; c < 3; ++c)
-                    xv[s][c] = *reinterpret_cast<const u32x4*>(xr + s * kXSlotBytes + k * kXBlockBytes + 16 * c);
+                    xv[s][c] = *reinterpret_cast<const u32x4*>(xr + s * kXSlotBytes + k * MxSets<B>::kBlock + 16 * c);
             __builtin_amdgcn_sched_barrier(0);
             uint32_t y[12];
             const uint32_t sa = block_values(st.cur, y);
@@ -851,7 +867,7 @@ __device__ __forceinline__ void run_piece_mx(const GemvProblem& P, Piece& pc, co
     constexpr int NS = MxSets<B>::kN;
     const int lane = threadIdx.x & 63;
     const uint8_t* tb = P.codes + static_cast<size_t>(pc.t) * P.nblk * kChunk;
-    const uint8_t* xr = xs + 48 * (threadIdx.x & 3);
+    const uint8_t* xr = xs + MxSets<B>::kRow * (threadIdx.x & 3);
     const int jg = pc.jg;
     int j = pc.j;
     int kb = pc.c0 - 4 * j;
