@@ -652,9 +652,9 @@ def main_encode(args, torch, tt):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU: the fused GEMV has no multi-GPU path in "
-              "this build (rows shard without communication; see the design notes). "
-              "Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (a "
+              "matrix's row tiles would shard over GPUs without communication, each "
+              "GPU producing its own rows of y). Run with --gpus 1.", file=sys.stderr)
         return 2
     import torch
     import paper_2609_35465_amd as tt

@@ -54,7 +54,7 @@ typedef enum {
     TETRA_EINVAL = -1,       /* null pointer, size out of range, bad batch  */
     TETRA_EALIGN = -2,       /* a device pointer is not aligned as required */
     TETRA_EDEVICE = -3,      /* HIP runtime error (table upload or launch)  */
-    TETRA_EUNSUPPORTED = -4  /* valid request this build does not serve     */
+    TETRA_EUNSUPPORTED = -4  /* valid request the library does not serve    */
 } tetra_status;
 
 /* Rows of one code tile of the device layout (see tetra_pack_rows). */
