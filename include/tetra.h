@@ -13,7 +13,7 @@
  * Conventions fixed by this library where the paper is silent (the word bit
  * layout, the trellis numbering, the rank-table tie-break, the value order
  * for o = 2 and the gain values) are the canonical ones returned by
- * tetra_get_tables() and documented with the design notes.
+ * tetra_get_tables().
  *
  * Canonical 48-bit word, stored as 6 little-endian bytes:
  *     bits 0-5 s8 | 6 p | 7 r | 8 b1 | 9-12 b2 | 13 b3 | 14 g |
@@ -214,10 +214,12 @@ int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x,
  * Eq. 2): for each block the canonical word of the kept lattice point whose
  * direction is closest among the nearest kept points to r * w / ||w|| at
  * the two trial radii r = radius0, radius1, and the gain bit nearest to the
- * block's projection on it.  Scores are exact integers (targets on a grid of
- * 2^-16, see the design notes for the full definition and its tie rules), so
- * the result is fixed by the inputs.  A block whose squared norm is zero or
- * not finite gets the word 0.
+ * block's projection on it.  Scores are exact integers: with targets
+ * T_j = rint(w_j r 2^16 / ||w||), a kept point y scores
+ * S(y) = sum_j (2 T_j y_j - 2^16 y_j^2); equal scores go to the first row
+ * of a section's list and then to the smallest trellis key, and equal
+ * projections to the first radius, so the result is fixed by the inputs.
+ * A block whose squared norm is zero or not finite gets the word 0.
  *   w:         device fp32 [n][24], block order (coordinate j of a block
  *              multiplies activation 24 blk + j), 4-byte aligned
  *   sigma:     device fp32 [n], the row scale of each block's row
