@@ -49,7 +49,8 @@ class Packed:
     def gemv(self, x):
         batch = x.shape[0]
         xd = _f16_dev(x)
-        y = torch.empty((batch, self.M), dtype=torch.float32, device="cuda")
+        # NaN-filled, so that a row the kernel never writes cannot pass
+        y = torch.full((batch, self.M), float("nan"), dtype=torch.float32, device="cuda")
         tt.gemv(self.blob, self.sigma, xd, y, self.M, self.K, batch)
         torch.cuda.synchronize()
         return y.cpu().numpy()
@@ -98,6 +99,27 @@ def test_decode_bit_exact(n):
     yo, _, so = codec.decode(words)
     assert np.array_equal(y.cpu().numpy(), yo)
     assert np.array_equal(s.cpu().numpy().view(np.uint32), so.view(np.uint32))
+
+
+@pytest.mark.parametrize("chunk", range(10))
+def test_decode_bit_exact_ten_million_words(chunk):
+    """10^7 distinct seeded random words in ten launches of 10^6, every
+    coordinate and block scale bit for bit (the paper's decoder cross-check,
+    Sec. 5.1)."""
+    n = 1_000_000
+    rng = np.random.default_rng(0xDEC0 + chunk)
+    words = rng.integers(0, 1 << 48, size=n, dtype=np.uint64)
+    wb = codec.words_to_bytes(words).reshape(-1)
+    y = torch.full((n, 24), 127, dtype=torch.int8, device="cuda")
+    s = torch.full((n,), float("nan"), dtype=torch.float32, device="cuda")
+    print(f"[decode] chunk {chunk} n={n}", flush=True)
+    tt.decode(_dev(wb), n, y, s)
+    torch.cuda.synchronize()
+    yg, sg = y.cpu().numpy(), s.cpu().numpy()
+    for i in range(0, n, 1 << 17):
+        yo, _, so = codec.decode(words[i:i + (1 << 17)])
+        assert np.array_equal(yg[i:i + (1 << 17)], yo)
+        assert np.array_equal(sg[i:i + (1 << 17)].view(np.uint32), so.view(np.uint32))
 
 
 def test_decode_without_scale_output():
@@ -307,23 +329,43 @@ def test_gemv_grouped_sixteen_problems():
         assert float((np.abs(y.cpu().numpy() - yr) / norm).max()) <= TOL_PAPER
 
 
-# ----------------------------------------- full-size configurations (sampled)
-
 def _sample_rows(M, rng, n=192):
     rows = set(range(min(M, 64))) | {M - 1, M - 2, M // 2}
     rows |= set(rng.choice(M, size=min(n, M), replace=False).tolist())
     return np.array(sorted(rows))
 
 
-@pytest.mark.parametrize("config,batch", [(0, 1), (1, 1), (2, 1), (3, 1), (3, 4)])
-def test_gemv_config_sampled_rows(config, batch):
-    rng = np.random.default_rng(config * 10 + batch)
-    for idx, (name, M, K) in enumerate(workloads.config_shapes(config)):
-        words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(config, idx), M, K)
-        pk = Packed(words, sigma, tail, K)
-        x = workloads.activations(workloads.seed_for(config, idx), batch, K)
-        _check_gemv(pk, x, rows=_sample_rows(M, rng), label=f"c{config}:{name}")
-        del pk
+# ------------------------------------------ full-size configurations (every row)
+
+def _config_cases():
+    cases = []
+    for config, batch in [(0, 1), (1, 1), (2, 1), (3, 1), (3, 4)]:
+        for idx, (name, M, K) in enumerate(workloads.config_shapes(config)):
+            cases.append(pytest.param(config, batch, idx, id=f"c{config}-b{batch}-{name}"))
+    return cases
+
+
+@pytest.mark.parametrize("config,batch,idx", _config_cases())
+def test_gemv_config_every_row(config, batch, idx):
+    """Every output row of one layer of each shape set (the single matrix,
+    the 4B, 8B and 14B sets at batch 1, the 14B set at batch 4) against the
+    oracle's float64 product, as the paper's kernel check recomputes every
+    row (Sec. 5.1).  The oracle runs in row chunks; y starts as NaN."""
+    name, M, K = workloads.config_shapes(config)[idx]
+    words, sigma, tail = workloads.tetra_matrix(workloads.seed_for(config, idx), M, K)
+    pk = Packed(words, sigma, tail, K)
+    x = workloads.activations(workloads.seed_for(config, idx), batch, K)
+    yg = pk.gemv(x).astype(np.float64)
+    worst = 0.0
+    for r0 in range(0, M, 4096):
+        rows = np.arange(r0, min(r0 + 4096, M))
+        yr, norm = ogemv.gemv_f64(words, sigma, tail, x, rows=rows)
+        err = np.abs(yg[:, rows] - yr) / np.maximum(norm, 1e-300)
+        assert not np.isnan(err).any(), (name, r0)
+        worst = max(worst, float(err.max()))
+        print(f"[gemv c{config}:{name} b{batch}] rows {r0}..{rows[-1]} worst so far {worst:.3e}", flush=True)
+    assert worst <= TOL
+    assert worst <= TOL_PAPER
 
 
 # ------------------------------------------------------------- determinism

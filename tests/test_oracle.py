@@ -580,3 +580,60 @@ def test_retention_formula():
     D = 2^-4 is a rate of 2 bits, retention 1; D = 1/4 gives 1/2."""
     assert encoder.retention(2.0 ** -4) == pytest.approx(1.0)
     assert encoder.retention(0.25) == pytest.approx(0.5)
+
+
+def test_encoder_is_nearest_to_the_scaled_direction_in_float64():
+    """Sec. 3.1, Eq. 2: at a trial radius a the search keeps the point y
+    nearest to t = a w / ||w||.  The oracle scores on a grid of 2^-16:
+    with T_j = 2^16 t_j + e_j and |e_j| <= 1/2, its score is
+    S(y) = 2^16 (||t||^2 - ||t - y||^2) + 2 e.y, so for the result y* and any
+    kept point y,  ||t - y*||^2 <= ||t - y||^2 + ||y* - y||_1 / 2^16.
+    Here that bound is checked with distances computed directly in float64
+    (not through S) against every word one field away from y* and 20,000
+    random words, for seeded Gaussian blocks at both trial radii."""
+    rng = np.random.default_rng(314)
+    sweeps = {"i1": 2048, "i2": 2048, "i3": 2048, "s8": 64, "b1": 2, "b2": 16, "b3": 2, "p": 2, "r": 2}
+    rand = codec.decode(rng.integers(0, 1 << 48, size=20000, dtype=np.uint64))[0].astype(np.float64)
+    for _ in range(3):
+        w = rng.standard_normal(24).astype(np.float32)
+        for a in (13.0, 15.0):
+            t = a * w.astype(np.float64) / np.sqrt((w.astype(np.float64) ** 2).sum())
+            _, f, y = encoder.nearest_point(encoder.targets(w, a))
+            ys = [rand]
+            for name, n in sweeps.items():
+                ff = dict(f, g=0)
+                ff[name] = np.arange(n)
+                ff = {k: np.broadcast_to(np.asarray(v), (n,)) for k, v in ff.items()}
+                ys.append(codec.decode(codec.pack_fields(**ff))[0].astype(np.float64))
+            ys = np.concatenate(ys)
+            ystar = y.astype(np.float64)
+            d_star = ((t - ystar) ** 2).sum()
+            d = ((t[None] - ys) ** 2).sum(axis=1)
+            slack = np.abs(ys - ystar[None]).sum(axis=1) / 2.0 ** 16 + 1e-9
+            assert (d_star <= d + slack).all()
+            # the grid term is rarely needed: almost every listed point is plainly farther
+            assert (d_star <= d + 1e-9).mean() > 0.999
+
+
+def test_reconstruct_is_the_shape_gain_block_and_matches_dequant():
+    """Eq. 2 for the encoder's reconstruction: a nonzero word gives a block
+    along its lattice point y with Euclidean norm gain[g] * sigma; the zero
+    point gives zeros; and it equals the dequantised weights
+    fl32(fl32(y s_blk) sigma) within their four fp32 roundings."""
+    rng = np.random.default_rng(2718)
+    words = rng.integers(0, 1 << 48, size=4000, dtype=np.uint64)
+    words[:4] = 0                                              # the origin, g = 0
+    sig16 = (rng.uniform(0.5, 2.0, words.size) * 1e-2).astype(np.float16)
+    rec = encoder.reconstruct(words, sig16.astype(np.float64))
+    y = codec.decode(words)[0].astype(np.float64)
+    g = codec.fields(words)["g"]
+    ny = np.sqrt((y * y).sum(axis=1))
+    nz = ny > 0
+    assert not nz[:4].any() and np.all(rec[~nz] == 0)
+    want = tables.gain().astype(np.float64)[g] * sig16.astype(np.float64)
+    assert np.allclose(np.sqrt((rec * rec).sum(axis=1))[nz], want[nz], rtol=1e-12, atol=0)
+    # along y: rec = c * y with one c per block
+    c = (rec * y).sum(axis=1)[nz] / (ny[nz] ** 2)
+    assert np.allclose(rec[nz], c[:, None] * y[nz], rtol=1e-12, atol=1e-300)
+    dq = gemv.dequant(words.reshape(-1, 1), sig16).astype(np.float64)
+    assert np.allclose(dq[nz], rec[nz], rtol=4 * 2.0 ** -24, atol=0)
