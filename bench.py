@@ -503,11 +503,12 @@ def main_prefill(args, torch, tt):
                 xs[K] = torch.as_tensor(workloads.activations(0x7E7A_0070 + K, N, K)).cuda()
             mats.append((m, xs[K], torch.empty((N, M), dtype=torch.float32, device="cuda")))
     stream = torch.cuda.current_stream()
+    ws = tt.gemm_workspace()
 
     def step(s=None):
         st = (s or stream).cuda_stream
         for m, x, y in mats:
-            tt.gemm(m.blob, m.sigma, x, y, m.M, m.K, N, stream=st)
+            tt.gemm(m.blob, m.sigma, x, y, m.M, m.K, N, ws, stream=st)
 
     step()
     torch.cuda.synchronize()

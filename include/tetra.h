@@ -23,16 +23,17 @@
  * Memory: all buffers are owned by the caller.  "host" arguments are plain
  * host pointers; "device" arguments are device pointers on the current HIP
  * device (for example from hipMalloc or torch.empty(..., device="cuda")).
- * The library owns its constant decoder tables and two workspaces per
- * device: the GEMV's (a counter and two partial sums per workgroup, about
- * 3 MB on a 256-CU part) and tetra_gemm's (a counter and two 64 KB partial
- * sums per workgroup, about 64 MB), all set up on the first call on the
- * device (thread-safe; make that first call outside stream capture).  After
- * that, launching calls are asynchronous on the given stream, never
- * synchronise and never allocate.  A workspace is shared by the calls of a
- * device that use it: such calls on one device must not overlap in time
- * (issue them on one stream, or order the streams); the counters return to
- * zero at the end of every launch.
+ * No call allocates or frees memory, and none synchronises: the decoder
+ * tables are constant data of the library's code object, built when the
+ * library is built, and the GEMV workspaces (a counter and two partial sums
+ * per workgroup) are static device memory in 16 slots per device.  A stream
+ * takes a slot at its first GEMV call on a device and keeps it until
+ * tetra_release_stream; GEMV calls on different streams therefore never
+ * share a workspace and may run at the same time, and a 17th stream is
+ * refused with TETRA_EBUSY.  The first call on a device (any call,
+ * including one made while the stream is being captured into a graph) only
+ * queries device attributes on the host.  tetra_gemm takes its workspace
+ * from the caller.
  *
  * Errors: every call validates its arguments before any launch and returns
  * a tetra_status.  TETRA_EDEVICE reports a HIP error seen at launch time;
@@ -53,8 +54,9 @@ typedef enum {
     TETRA_OK = 0,
     TETRA_EINVAL = -1,       /* null pointer, size out of range, bad batch  */
     TETRA_EALIGN = -2,       /* a device pointer is not aligned as required */
-    TETRA_EDEVICE = -3,      /* HIP runtime error (table upload or launch)  */
-    TETRA_EUNSUPPORTED = -4  /* valid request the library does not serve    */
+    TETRA_EDEVICE = -3,      /* HIP runtime error (device query or launch)  */
+    TETRA_EUNSUPPORTED = -4, /* valid request the library does not serve    */
+    TETRA_EBUSY = -5         /* all GEMV workspace slots held by other streams */
 } tetra_status;
 
 /* Rows of one code tile of the device layout (see tetra_pack_rows). */
@@ -88,6 +90,15 @@ int tetra_get_tables(void* out, size_t bytes);
  * is odd.
  */
 size_t tetra_codes_bytes(int M, int K);
+
+/*
+ * Code bytes per row of an M x K matrix: 6 * (K / 24), 48 bits per block.
+ * Rows are not stored one after another: the device layout interleaves
+ * them in tiles of TETRA_ROW_TILE rows (see tetra_pack_rows), and tile t
+ * starts at byte t * TETRA_ROW_TILE * tetra_row_stride(K).  Returns 0 if
+ * K < 24 or K is odd.  Host only, pure.
+ */
+size_t tetra_row_stride(int K);
 
 /* Byte offset of the fp16 tail inside the code blob (0 if the shape is
  * invalid): the code chunks rounded up to 16 bytes. */
@@ -148,9 +159,11 @@ int tetra_unpack_rows(const void* codes, size_t codes_bytes, int M, int K,
  *   x:          device fp16[batch][K], 4-byte aligned
  *   y:          device fp32[batch][M], fully overwritten
  *   batch:      1..TETRA_MAX_BATCH
+ * Uses the GEMV workspace slot of `stream` (see Memory above).
  * Asynchronous on stream.  TETRA_EINVAL for NULL pointers, bad M/K, batch
- * out of range; TETRA_EALIGN for misaligned codes or x; TETRA_EDEVICE when
- * the table upload or the launch fails.
+ * out of range; TETRA_EALIGN for misaligned codes or x; TETRA_EBUSY when the
+ * stream has no slot and none is free; TETRA_EDEVICE when a device query or
+ * the launch fails.
  */
 int tetra_gemv(const void* codes, const uint16_t* row_scales, const uint16_t* x,
                float* y, int M, int K, int batch, hipStream_t stream);
@@ -202,12 +215,33 @@ int tetra_decode(const void* words, size_t n, int8_t* y_out, float* blk_scale_ou
  * tetra_gemv's (another summation order), within the same bound, and the
  * split of the work over workgroups follows M, K, N and the CU count, so a
  * token's result can change in the last bits with N (it never changes from
- * run to run).  Uses the device's product workspace: like GEMV calls, calls
- * on one device must not overlap in time.  Asynchronous; TETRA_EINVAL /
- * TETRA_EALIGN / TETRA_EDEVICE as for tetra_gemv.
+ * run to run).
+ *   workspace: device memory of the caller, 256-byte aligned, holding
+ *              counters and partial sums of the pieces of a launch; it
+ *              must be zero-filled before its first use, and every call
+ *              leaves it zero-filled again.  Calls that may run at the
+ *              same time need different workspaces.
+ *   workspace_bytes: its size; tetra_gemm_workspace_bytes() is the size at
+ *              which the product uses every workgroup the device holds (a
+ *              smaller workspace runs fewer workgroups, TETRA_EINVAL below
+ *              one workgroup's share)
+ * Asynchronous; TETRA_EINVAL / TETRA_EALIGN / TETRA_EDEVICE as for
+ * tetra_gemv.
  */
 int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
-               hipStream_t stream);
+               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes at which tetra_gemm uses the whole current device (host
+ * only; 0 when the device cannot be queried). */
+size_t tetra_gemm_workspace_bytes(void);
+
+/*
+ * Gives back the GEMV workspace slot that `stream` holds on the current
+ * device, if any (host only).  Call it only when no GEMV work issued on the
+ * stream is still pending or will be replayed from a graph.  Always
+ * TETRA_OK unless the device cannot be queried.
+ */
+int tetra_release_stream(hipStream_t stream);
 
 /*
  * Encoder of 24-weight blocks (the offline step of Sec. 3.1, shape-gain of

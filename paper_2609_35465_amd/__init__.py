@@ -15,7 +15,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtetra.so")
 
-OK, EINVAL, EALIGN, EDEVICE, EUNSUPPORTED = 0, -1, -2, -3, -4
+OK, EINVAL, EALIGN, EDEVICE, EUNSUPPORTED, EBUSY = 0, -1, -2, -3, -4, -5
 ROW_TILE = 64
 TABLE_BLOB_BYTES = 18824
 MAX_BATCH = 8
@@ -30,6 +30,7 @@ _SIGNATURES = {
     "tetra_status_string": (ctypes.c_char_p, [_int]),
     "tetra_get_tables": (_int, [_vp, _sz]),
     "tetra_codes_bytes": (_sz, [_int, _int]),
+    "tetra_row_stride": (_sz, [_int]),
     "tetra_tail_offset": (_sz, [_int, _int]),
     "tetra_pack_rows": (_int, [_vp, _vp, _int, _int, _vp, _sz]),
     "tetra_unpack_rows": (_int, [_vp, _sz, _int, _int, _vp, _vp]),
@@ -40,7 +41,9 @@ _SIGNATURES = {
     "tetra_int4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_head4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_rotate": (_int, [_vp, _vp, _vp, _int, _int, _int, _vp]),
-    "tetra_gemm": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
+    "tetra_gemm": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp, _sz, _vp]),
+    "tetra_gemm_workspace_bytes": (_sz, []),
+    "tetra_release_stream": (_int, [_vp]),
     "tetra_emb4_gather": (_int, [_vp, _vp, _int, _int, _vp, _int, _vp, _vp]),
     "tetra_encode": (_int, [_vp, _vp, _sz, ctypes.c_double, ctypes.c_double, _vp, _vp]),
 }
@@ -96,6 +99,10 @@ def codes_bytes(M: int, K: int) -> int:
     return int(_call("tetra_codes_bytes", M, K))
 
 
+def row_stride(K: int) -> int:
+    return int(_call("tetra_row_stride", K))
+
+
 def tail_offset(M: int, K: int) -> int:
     return int(_call("tetra_tail_offset", M, K))
 
@@ -144,10 +151,32 @@ def gemv(codes, row_scales, x, y, M: int, K: int, batch: int = 1, stream=None):
                      _stream(stream)), "tetra_gemv")
 
 
-def gemm(codes, row_scales, x, y, M: int, K: int, N: int, stream=None):
-    """y[N, M] = W x for N activation rows (a prompt), on the matrix cores."""
-    _check(_call("tetra_gemm", _ptr(codes), _ptr(row_scales), _ptr(x), _ptr(y), M, K, N, _stream(stream)),
-           "tetra_gemm")
+def gemm_workspace_bytes() -> int:
+    """Workspace bytes at which tetra_gemm uses the whole current device."""
+    return int(_call("tetra_gemm_workspace_bytes"))
+
+
+def gemm_workspace():
+    """A zero-filled workspace for tetra_gemm on the current device (a torch
+    uint8 tensor; torch allocates it, 256-byte aligned)."""
+    import torch
+    n = gemm_workspace_bytes()
+    if n == 0:
+        raise TetraError(EDEVICE, "tetra_gemm_workspace_bytes")
+    return torch.zeros(n, dtype=torch.uint8, device="cuda")
+
+
+def gemm(codes, row_scales, x, y, M: int, K: int, N: int, workspace, stream=None):
+    """y[N, M] = W x for N activation rows (a prompt), on the matrix cores;
+    workspace from gemm_workspace() (one per stream that runs products at
+    the same time as others)."""
+    _check(_call("tetra_gemm", _ptr(codes), _ptr(row_scales), _ptr(x), _ptr(y), M, K, N, _ptr(workspace),
+                 int(workspace.numel() * workspace.element_size()), _stream(stream)), "tetra_gemm")
+
+
+def release_stream(stream=None):
+    """Gives back the GEMV workspace slot that the stream holds on the current device."""
+    _check(_call("tetra_release_stream", _stream(stream)), "tetra_release_stream")
 
 
 def encode(w, sigma, n: int, words_out, radii=None, stream=None):

@@ -37,10 +37,41 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+BUILD_DIR = os.path.join(HERE, "_build")
+GEN_SOURCES = ["gen_tables.cpp", "tables.cpp"]
+
+
+def _run(cmd, verbose, **kw):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True, **kw)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"{cmd[0]} failed with status {res.returncode}")
+    return res
+
+
+def generate_tables(verbose: bool = False) -> str:
+    """Builds and runs the host table generator; writes the initialisers of
+    the device decoder tables to _build/tables_data.inc and returns the
+    directory."""
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    gen = os.path.join(BUILD_DIR, "gen_tables")
+    _run([hipcc(), "-O2", "-std=c++17", "-Wno-unused-command-line-argument",
+          *[os.path.join(CSRC, s) for s in GEN_SOURCES], "-o", gen], verbose)
+    out = _run([gen], verbose).stdout
+    path = os.path.join(BUILD_DIR, "tables_data.inc")
+    with open(path + ".tmp", "w") as f:
+        f.write(out)
+    os.replace(path + ".tmp", path)
+    return BUILD_DIR
+
+
 def build(verbose: bool = False) -> str:
     """Compiles every source into libtetra.so next to this file; returns its path."""
+    inc = generate_tables(verbose)
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIP_FLAGS, *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+    cmd = [hipcc(), *HIP_FLAGS, "-I", inc, *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -293,10 +293,27 @@ struct GemvGroup {
     GemvProblem prob[kMaxGroup];
     double inv_total, inv_waves;   // 1 / total, 1 / waves
     uint32_t total;                // blocks in the launch sequence (< 2^31)
-    uint32_t* counters;            // [groups], zero between launches
-    float* partials;               // [groups][2][B][64]
+    int slot;                      // workspace slot of the launch (g_gemv_slots)
     int n, waves;
 };
+
+// GEMV workspaces: a counter and two partial sums per workgroup.  One slot
+// per stream that issues GEMV calls on a device, so that calls on different
+// streams never share one; static device memory, zero when the code object
+// loads, and every launch leaves its counters at zero again.  A slot covers
+// kGemvMaxGroups workgroups, and its partial sums [groups][2][B][64] the
+// largest batch at one workgroup per CU or batch 2 at two.
+constexpr int kGemvSlots = 16;
+constexpr int kGemvMaxCUs = 320;
+constexpr int kGemvMaxGroups = kGemvMaxCUs * kGemvGroupsPerCU;
+constexpr int kGemvSlotPartials = kGemvMaxCUs * 2 * 8 * 64;
+
+struct GemvSlot {
+    uint32_t counters[kGemvMaxGroups];
+    float partials[kGemvSlotPartials];
+};
+
+__device__ GemvSlot g_gemv_slots[kGemvSlots];
 
 // wave count of a launch: one round of the 768-thread workgroups a CU holds
 // at once (`groups`: two at batch 1 and 2; one from batch 3 on, whose
@@ -312,10 +329,10 @@ inline int gemv_waves(uint32_t total, int cus, int groups) {
     return static_cast<int>(want < cap ? want : cap);
 }
 
-// workspace bytes for G workgroups at batch B: a counter and two partial
-// sums per workgroup
-inline size_t gemv_workspace_bytes(int G, int B) {
-    return static_cast<size_t>(G) * sizeof(uint32_t) + static_cast<size_t>(G) * 2 * B * 64 * sizeof(float);
+// largest workgroup count of a launch at batch B that the slot's partial
+// sums hold
+constexpr int gemv_max_groups(int B) {
+    return kGemvSlotPartials / (2 * B * 64) < kGemvMaxGroups ? kGemvSlotPartials / (2 * B * 64) : kGemvMaxGroups;
 }
 
 // floor(n / d) for n < 2^53, from a reciprocal of d computed on the host
@@ -986,6 +1003,8 @@ void gemv_kernel(const GemvGroup grp) {
     ts.load();
     uint32_t i = __builtin_amdgcn_readfirstlane(range_begin(w, grp));
     const uint32_t end = __builtin_amdgcn_readfirstlane(range_begin(w + 1, grp));
+    uint32_t* const counters = g_gemv_slots[grp.slot].counters;
+    float* const partials = g_gemv_slots[grp.slot].partials;
     int p = 0;
     while (p + 1 < grp.n && i >= grp.prob[p + 1].blk_base) ++p;
     const uint32_t rel = i - grp.prob[p].blk_base;
@@ -1058,14 +1077,14 @@ void gemv_kernel(const GemvGroup grp) {
                     const int gslot_ga =
                         __builtin_amdgcn_readfirstlane(range_begin(ga * kGemvWaves, grp) >= t0 ? 0 : 1);
                     auto gslot_of = [&](int h) { return h > ga ? 0 : gslot_ga; };
-                    float* gp = grp.partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + ln;
+                    float* gp = partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + ln;
 #pragma unroll
                     for (int bb = 0; bb < B; ++bb)
                         __hip_atomic_store(gp + bb * 64, tot[bb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
                     uint32_t garr = 0;
                     if (ln == 0)
-                        garr = __hip_atomic_fetch_add(grp.counters + gb, 1u, __ATOMIC_RELAXED,
+                        garr = __hip_atomic_fetch_add(counters + gb, 1u, __ATOMIC_RELAXED,
                                                       __HIP_MEMORY_SCOPE_AGENT);
                     garr = __builtin_amdgcn_readfirstlane(garr);
                     if (garr == static_cast<uint32_t>(gb - ga)) {
@@ -1079,7 +1098,7 @@ void gemv_kernel(const GemvGroup grp) {
                                 const int h = h0 + u;
                                 if (h <= gb) {
                                     const float* ph =
-                                        grp.partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + ln;
+                                        partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + ln;
 #pragma unroll
                                     for (int bb = 0; bb < B; ++bb)
                                         pv[u][bb] = __hip_atomic_load(ph + bb * 64, __ATOMIC_RELAXED,
@@ -1094,7 +1113,7 @@ void gemv_kernel(const GemvGroup grp) {
                                 }
                         }
                         if (ln == 0)
-                            __hip_atomic_store(grp.counters + gb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            __hip_atomic_store(counters + gb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                         store_rows<B>(P, t, tot, rt);
                     }
                 }

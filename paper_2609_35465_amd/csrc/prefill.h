@@ -93,10 +93,13 @@ __device__ __forceinline__ uint32_t pf_slot_bytes(int worker, int side) {
     return static_cast<uint32_t>((worker * 2 + side) * kPfSlot) * 4u;
 }
 
-// workspace of a launch with at most `workers` workgroups
+// workspace of a launch with at most `workers` workgroups: the counters
+// (rounded up to 256 bytes), then two piece slots per workgroup
+inline size_t gemm_counter_bytes(int workers) {
+    return (sizeof(uint32_t) * static_cast<size_t>(workers) + 255) & ~static_cast<size_t>(255);
+}
 inline size_t gemm_workspace_bytes(int workers) {
-    return sizeof(uint32_t) * static_cast<size_t>(workers) +
-           sizeof(float) * static_cast<size_t>(workers) * 2 * kPfSlot;
+    return gemm_counter_bytes(workers) + sizeof(float) * static_cast<size_t>(workers) * 2 * kPfSlot;
 }
 
 // a workgroup-uniform 64-bit value in scalar registers (the 64-bit divisions

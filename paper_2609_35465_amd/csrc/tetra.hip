@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cstring>
 #include <mutex>
+#include <thread>
 #include <vector>
 
 #include "../../include/tetra.h"
@@ -27,22 +28,21 @@ using tetra_dev::kTile;
 
 constexpr int kMaxDevices = 64;
 
-std::mutex g_init_mu;
-bool g_init_done[kMaxDevices];
-
-// Per-device workspaces of the GEMV and of the many-token product (counters
-// and partial sums of pieces of tiles or items), allocated and zeroed with the
-// tables; the counters are back at zero after every launch.
-struct Workspace {
-    uint32_t* counters = nullptr;
-    float* partials = nullptr;
-    int max_waves = 0;
-    uint32_t* gemm_counters = nullptr;
-    float* gemm_partials = nullptr;
+// What the host knows about a device, queried once and kept: no call makes
+// the device do any work, allocate or wait to set it up.  Also the owners of
+// the device's GEMV workspace slots (kernels.h, g_gemv_slots).
+struct DeviceState {
+    bool ready = false;
+    int cus = 0;
+    int gemv_groups[TETRA_MAX_BATCH + 1] = {};   // resident GEMV workgroups per CU, by batch
     int gemm_workers = 0;
-    int gemv_groups[TETRA_MAX_BATCH + 1] = {};    // resident GEMV workgroups per CU, by batch
+    bool slot_used[tetra_dev::kGemvSlots] = {};
+    hipStream_t slot_stream[tetra_dev::kGemvSlots] = {};
+    std::thread::id slot_thread[tetra_dev::kGemvSlots];
 };
-Workspace g_ws[kMaxDevices];
+
+std::mutex g_mu;
+DeviceState g_dev[kMaxDevices];
 
 int num_cus(int dev) {
     int n = 0;
@@ -62,61 +62,63 @@ int gemv_resident() {
     return std::max(1, std::min(n, tetra_dev::kGemvGroupsPerCU));
 }
 
-int ensure_tables(int* dev_out) {
+// the current device and its state (filled on first use); called with g_mu held
+int device_state_locked(int* dev_out, DeviceState** out) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TETRA_EDEVICE;
     *dev_out = dev;
-    std::lock_guard<std::mutex> lk(g_init_mu);
-    if (g_init_done[dev]) return TETRA_OK;
-    const tetra::HostTables* T = nullptr;
-    try {
-        T = &tetra::host_tables();
-    } catch (...) {
-        return TETRA_EDEVICE;
+    DeviceState& d = g_dev[dev];
+    if (!d.ready) {
+        static_assert(TETRA_MAX_BATCH == 8, "one residency entry per batch size");
+        const int resident[TETRA_MAX_BATCH + 1] = {0, gemv_resident<1>(), gemv_resident<2>(), gemv_resident<3>(),
+                                                   gemv_resident<4>(), gemv_resident<5>(), gemv_resident<6>(),
+                                                   gemv_resident<7>(), gemv_resident<8>()};
+        for (int b = 1; b <= TETRA_MAX_BATCH; ++b)
+            if (resident[b] == 0) return TETRA_EDEVICE;
+        d.cus = num_cus(dev);
+        for (int b = 0; b <= TETRA_MAX_BATCH; ++b) d.gemv_groups[b] = resident[b];
+        d.gemm_workers = d.cus * tetra_dev::kPfGroupsPerCU;
+        d.ready = true;
     }
-    std::vector<uint8_t> buf(std::max(sizeof(tetra_dev::CanonicalTables), sizeof(tetra_dev::PackedTables)));
-    auto* c = reinterpret_cast<tetra_dev::CanonicalTables*>(buf.data());
-    tetra_dev::build_canonical(*T, c);
-    if (hipMemcpyToSymbol(HIP_SYMBOL(tetra_dev::g_canonical), c, sizeof(*c), 0, hipMemcpyHostToDevice) !=
-        hipSuccess)
-        return TETRA_EDEVICE;
-    auto* pk = reinterpret_cast<tetra_dev::PackedTables*>(buf.data());
-    tetra_dev::build_packed(*T, pk);
-    if (hipMemcpyToSymbol(HIP_SYMBOL(tetra_dev::g_packed), pk, sizeof(*pk), 0, hipMemcpyHostToDevice) !=
-        hipSuccess)
-        return TETRA_EDEVICE;
-    static_assert(TETRA_MAX_BATCH == 8, "one residency entry per batch size");
-    const int resident[TETRA_MAX_BATCH + 1] = {0, gemv_resident<1>(), gemv_resident<2>(), gemv_resident<3>(),
-                                               gemv_resident<4>(), gemv_resident<5>(), gemv_resident<6>(),
-                                               gemv_resident<7>(), gemv_resident<8>()};
-    for (int b = 1; b <= TETRA_MAX_BATCH; ++b)
-        if (resident[b] == 0) return TETRA_EDEVICE;
-    // both workspaces, zeroed; on any failure nothing stays allocated and the
-    // next call tries again
-    const int max_waves = num_cus(dev) * tetra_dev::kGemvGroupsPerCU * tetra_dev::kGemvWaves;
-    const int max_groups = max_waves / tetra_dev::kGemvWaves;
-    const size_t ws_bytes = tetra_dev::gemv_workspace_bytes(max_groups, TETRA_MAX_BATCH);
-    const int gemm_workers = num_cus(dev) * tetra_dev::kPfGroupsPerCU;
-    const size_t gemm_bytes = tetra_dev::gemm_workspace_bytes(gemm_workers);
-    void* mem = nullptr;
-    void* gmem = nullptr;
-    if (hipMalloc(&mem, ws_bytes) != hipSuccess || hipMalloc(&gmem, gemm_bytes) != hipSuccess ||
-        hipMemset(mem, 0, ws_bytes) != hipSuccess || hipMemset(gmem, 0, gemm_bytes) != hipSuccess ||
-        hipDeviceSynchronize() != hipSuccess) {
-        if (mem) (void)hipFree(mem);
-        if (gmem) (void)hipFree(gmem);
-        return TETRA_EDEVICE;
+    *out = &d;
+    return TETRA_OK;
+}
+
+int device_state(int* dev_out, DeviceState* copy) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    DeviceState* d = nullptr;
+    if (int st = device_state_locked(dev_out, &d)) return st;
+    if (copy) *copy = *d;
+    return TETRA_OK;
+}
+
+// The per-thread default stream is a different stream in every thread.
+bool same_stream(const DeviceState& d, int i, hipStream_t s) {
+    return d.slot_stream[i] == s && (s != hipStreamPerThread || d.slot_thread[i] == std::this_thread::get_id());
+}
+
+// the GEMV workspace slot of `stream` on the current device, taking a free
+// one on the stream's first call; TETRA_EBUSY when all are held by others
+int gemv_slot(hipStream_t stream, DeviceState* copy, int* slot) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev;
+    DeviceState* d = nullptr;
+    if (int st = device_state_locked(&dev, &d)) return st;
+    int free_slot = -1;
+    for (int i = 0; i < tetra_dev::kGemvSlots; ++i) {
+        if (d->slot_used[i] && same_stream(*d, i, stream)) {
+            *slot = i;
+            *copy = *d;
+            return TETRA_OK;
+        }
+        if (!d->slot_used[i] && free_slot < 0) free_slot = i;
     }
-    Workspace& ws = g_ws[dev];
-    ws.max_waves = max_waves;
-    for (int b = 0; b <= TETRA_MAX_BATCH; ++b) ws.gemv_groups[b] = resident[b];
-    ws.counters = static_cast<uint32_t*>(mem);
-    ws.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(mem) + sizeof(uint32_t) * max_groups);
-    ws.gemm_workers = gemm_workers;
-    ws.gemm_counters = static_cast<uint32_t*>(gmem);
-    ws.gemm_partials =
-        reinterpret_cast<float*>(static_cast<uint8_t*>(gmem) + sizeof(uint32_t) * static_cast<size_t>(gemm_workers));
-    g_init_done[dev] = true;
+    if (free_slot < 0) return TETRA_EBUSY;
+    d->slot_used[free_slot] = true;
+    d->slot_stream[free_slot] = stream;
+    d->slot_thread[free_slot] = std::this_thread::get_id();
+    *slot = free_slot;
+    *copy = *d;
     return TETRA_OK;
 }
 
@@ -169,16 +171,19 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t s
         total += static_cast<unsigned long long>(s.tiles) * s.nblk;
     }
     if (total >= (1ull << 31)) return TETRA_EINVAL;     // block indices are 32-bit
-    int dev;
-    if (int st = ensure_tables(&dev)) return st;
-    const Workspace& ws = g_ws[dev];
+    DeviceState ds;
+    int slot = 0;
+    if (int st = gemv_slot(stream, &ds, &slot)) return st;
     grp.n = n;
     grp.total = static_cast<uint32_t>(total);
-    grp.waves = std::min(tetra_dev::gemv_waves(grp.total, num_cus(dev), ws.gemv_groups[batch]), ws.max_waves);
+    // the workspace slot holds kGemvMaxCUs CUs' worth of workgroups: a larger
+    // part runs fewer waves
+    const int cus = std::min(ds.cus, tetra_dev::kGemvMaxCUs);
+    grp.waves = std::min(tetra_dev::gemv_waves(grp.total, cus, ds.gemv_groups[batch]),
+                         tetra_dev::gemv_max_groups(batch) * tetra_dev::kGemvWaves);
     grp.inv_total = 1.0 / static_cast<double>(grp.total);
     grp.inv_waves = 1.0 / static_cast<double>(grp.waves);
-    grp.counters = ws.counters;
-    grp.partials = ws.partials;
+    grp.slot = slot;
     const int grid = (grp.waves + tetra_dev::kGemvWaves - 1) / tetra_dev::kGemvWaves;
 #define TETRA_LAUNCH(B)                                                                           \
     case B:                                                                                       \
@@ -208,14 +213,15 @@ int int4_gemv_launch(const void* q, const uint16_t* scale_off, const uint16_t* x
     if (batch < 1 || batch > TETRA_MAX_BATCH) return TETRA_EINVAL;
     if (!aligned(q, 8) || !aligned(scale_off, 4) || !aligned(x, 16)) return TETRA_EALIGN;
     int dev;
-    if (int st = ensure_tables(&dev)) return st;
+    DeviceState ds;
+    if (int st = device_state(&dev, &ds)) return st;
     const long long pairs = (static_cast<long long>(M) + tetra_dev::kInt4RowsPerWave - 1) / tetra_dev::kInt4RowsPerWave;
     const long long grid = (pairs + tetra_dev::kInt4Waves - 1) / tetra_dev::kInt4Waves;
     if (grid > 0x7FFFFFFFLL) return TETRA_EINVAL;
     const uint8_t* qb = static_cast<const uint8_t*>(q);
     // a launch of at least one row pair per wave of a full chip of persistent
     // workgroups stages the activations in LDS (when they fit in 64 KB)
-    const long long lds_groups = static_cast<long long>(tetra_dev::int4_lds_groups_per_cu(batch)) * num_cus(dev);
+    const long long lds_groups = static_cast<long long>(tetra_dev::int4_lds_groups_per_cu(batch)) * ds.cus;
     const size_t lds = tetra_dev::int4_lds_bytes(K, batch);
     const bool use_lds = batch <= tetra_dev::kInt4LdsMaxBatch &&
                          pairs >= lds_groups * tetra_dev::kInt4LdsWaves && lds <= 65536;
@@ -251,6 +257,7 @@ const char* tetra_status_string(int status) {
         case TETRA_EALIGN: return "misaligned device pointer";
         case TETRA_EDEVICE: return "HIP runtime error";
         case TETRA_EUNSUPPORTED: return "unsupported request";
+        case TETRA_EBUSY: return "every GEMV workspace slot of the device is held by another stream";
         default: return "unknown status";
     }
 }
@@ -265,6 +272,11 @@ int tetra_get_tables(void* out, size_t bytes) {
         return TETRA_EDEVICE;
     }
     return TETRA_OK;
+}
+
+size_t tetra_row_stride(int K) {
+    Shape s;
+    return shape_of(1, K, &s) ? static_cast<size_t>(s.nblk) * 6 : 0;
 }
 
 size_t tetra_codes_bytes(int M, int K) {
@@ -351,8 +363,9 @@ int tetra_decode(const void* words, size_t n, int8_t* y_out, float* blk_scale_ou
     if (!aligned(words, 2) || !aligned(y_out, 4) || (blk_scale_out && !aligned(blk_scale_out, 4)))
         return TETRA_EALIGN;
     int dev;
-    if (int st = ensure_tables(&dev)) return st;
-    const size_t blocks = std::min<size_t>((n + 255) / 256, static_cast<size_t>(num_cus(dev)) * 8);
+    DeviceState ds;
+    if (int st = device_state(&dev, &ds)) return st;
+    const size_t blocks = std::min<size_t>((n + 255) / 256, static_cast<size_t>(ds.cus) * 8);
     hipLaunchKernelGGL(tetra_dev::decode_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream,
                        static_cast<const uint16_t*>(words), n, y_out, blk_scale_out);
     return launch_status();
@@ -364,9 +377,10 @@ int tetra_dequant(const void* codes, const uint16_t* row_scales, int M, int K, f
     if (!codes || !row_scales || !w_out || !shape_of(M, K, &s)) return TETRA_EINVAL;
     if (!aligned(codes, 16) || !aligned(w_out, 4)) return TETRA_EALIGN;
     int dev;
-    if (int st = ensure_tables(&dev)) return st;
+    DeviceState ds;
+    if (int st = device_state(&dev, &ds)) return st;
     const size_t units = static_cast<size_t>(s.tiles) * s.nblk;
-    const size_t blocks = std::min<size_t>((units + 3) / 4, static_cast<size_t>(num_cus(dev)) * 2);
+    const size_t blocks = std::min<size_t>((units + 3) / 4, static_cast<size_t>(ds.cus) * 2);
     hipLaunchKernelGGL(tetra_dev::dequant_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256),
                        0, stream,
                        static_cast<const uint8_t*>(codes), row_scales, M, K, s.nblk, s.T,
@@ -388,7 +402,7 @@ namespace {
 
 // one launch of the many-token product over tokens n_base .. n_base + N - 1
 int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
-                const Shape& s, const Workspace& ws, hipStream_t stream) {
+                const Shape& s, int max_workers, uint8_t* workspace, hipStream_t stream) {
     const long long token_groups = (static_cast<long long>(N) + tetra_dev::kPfTokens - 1) / tetra_dev::kPfTokens;
     // four token groups per wave (items of two tiles) unless that cuts the
     // average item into more than eight pieces over the launch's workgroups;
@@ -396,7 +410,7 @@ int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t
     const int upi = s.nblk / tetra::kGroupCols + (s.nblk % tetra::kGroupCols ? 1 : 0);
     long long items = static_cast<long long>((s.tiles + 1) / 2) * token_groups;
     int tg = 4;
-    if (std::min<long long>(items * upi, ws.gemm_workers) > 8 * items) {
+    if (std::min<long long>(items * upi, max_workers) > 8 * items) {
         tg = 2;
         items = static_cast<long long>(s.tiles) * token_groups;
     }
@@ -421,12 +435,12 @@ int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t
     // at most eight workgroups per item on average: past that, a few more
     // chunks per workgroup cost less than the longer reduction
     a.workers = static_cast<int>(std::min<unsigned long long>(
-        std::min<unsigned long long>(a.units, static_cast<unsigned long long>(ws.gemm_workers)),
+        std::min<unsigned long long>(a.units, static_cast<unsigned long long>(max_workers)),
         static_cast<unsigned long long>(items) * 8));
     if (a.units > ~0ull / static_cast<unsigned long long>(a.workers + 1)) return TETRA_EINVAL;   // range arithmetic
-    a.counters = ws.gemm_counters;
-    a.partials = ws.gemm_partials;
-    a.partial_bytes = static_cast<int>(sizeof(float) * 2 * tetra_dev::kPfSlot * static_cast<size_t>(ws.gemm_workers));
+    a.counters = reinterpret_cast<uint32_t*>(workspace);
+    a.partials = reinterpret_cast<float*>(workspace + tetra_dev::gemm_counter_bytes(max_workers));
+    a.partial_bytes = static_cast<int>(sizeof(float) * 2 * tetra_dev::kPfSlot * static_cast<size_t>(max_workers));
     if (tg == 4)
         hipLaunchKernelGGL(tetra_dev::gemm_kernel<4>, dim3(static_cast<unsigned>(a.workers)),
                            dim3(tetra_dev::kPfThreads), 0, stream, a);
@@ -438,14 +452,28 @@ int gemm_launch(const uint8_t* codes, const uint16_t* row_scales, const uint16_t
 
 }  // namespace
 
-int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
-               hipStream_t stream) {
-    if (!codes || !row_scales || !x || !y || M < 1 || K < 24 || N < 1 || K % 8) return TETRA_EINVAL;
-    if (!aligned(codes, 16) || !aligned(x, 16) || !aligned(row_scales, 2) || !aligned(y, 4)) return TETRA_EALIGN;
+size_t tetra_gemm_workspace_bytes(void) {
     int dev;
-    if (int st = ensure_tables(&dev)) return st;
+    DeviceState ds;
+    if (device_state(&dev, &ds)) return 0;
+    return tetra_dev::gemm_workspace_bytes(ds.gemm_workers);
+}
+
+int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K, int N,
+               void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (!codes || !row_scales || !x || !y || !workspace || M < 1 || K < 24 || N < 1 || K % 8) return TETRA_EINVAL;
+    if (!aligned(codes, 16) || !aligned(x, 16) || !aligned(row_scales, 2) || !aligned(y, 4) ||
+        !aligned(workspace, 256))
+        return TETRA_EALIGN;
+    int dev;
+    DeviceState ds;
+    if (int st = device_state(&dev, &ds)) return st;
     Shape s;
     if (!shape_of(M, K, &s)) return TETRA_EINVAL;
+    // as many workgroups as the device holds and the workspace has slots for
+    int workers = ds.gemm_workers;
+    while (workers > 0 && tetra_dev::gemm_workspace_bytes(workers) > workspace_bytes) --workers;
+    if (workers < 1) return TETRA_EINVAL;
     // the kernel addresses a launch's activations with 32-bit byte offsets:
     // prompts longer than that run as several launches of whole token groups
     const long long slice = std::max<long long>(
@@ -454,9 +482,19 @@ int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x,
     for (long long n = 0; n < N; n += slice) {
         const int cnt = static_cast<int>(std::min<long long>(slice, N - n));
         if (int st = gemm_launch(static_cast<const uint8_t*>(codes), row_scales, x + n * K, y + n * M, M, K, cnt, s,
-                                 g_ws[dev], stream))
+                                 workers, static_cast<uint8_t*>(workspace), stream))
             return st;
     }
+    return TETRA_OK;
+}
+
+int tetra_release_stream(hipStream_t stream) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev;
+    DeviceState* d = nullptr;
+    if (int st = device_state_locked(&dev, &d)) return st;
+    for (int i = 0; i < tetra_dev::kGemvSlots; ++i)
+        if (d->slot_used[i] && same_stream(*d, i, stream)) d->slot_used[i] = false;
     return TETRA_OK;
 }
 
@@ -467,7 +505,8 @@ int tetra_encode(const float* w, const float* sigma, size_t n, double radius0, d
         if (!(r > 0.0 && r <= tetra_dev::kEncMaxRadius)) return TETRA_EINVAL;
     if (!aligned(w, 4) || !aligned(sigma, 4) || !aligned(words_out, 2)) return TETRA_EALIGN;
     int dev;
-    if (int st = ensure_tables(&dev)) return st;
+    DeviceState ds;
+    if (int st = device_state(&dev, &ds)) return st;
     tetra_dev::EncodeArgs a;
     a.w = w;
     a.sigma = sigma;
@@ -475,7 +514,7 @@ int tetra_encode(const float* w, const float* sigma, size_t n, double radius0, d
     a.n = n;
     a.alpha[0] = radius0;
     a.alpha[1] = radius1;
-    const size_t grid = std::min<size_t>(n, static_cast<size_t>(num_cus(dev)) * 8);
+    const size_t grid = std::min<size_t>(n, static_cast<size_t>(ds.cus) * 8);
     hipLaunchKernelGGL(tetra_dev::encode_kernel, dim3(static_cast<unsigned>(grid)), dim3(tetra_dev::kEncThreads), 0,
                        stream, a);
     return launch_status();
@@ -487,7 +526,8 @@ int tetra_rotate(const uint16_t* x, const uint8_t* sign_bits, uint16_t* out, int
     if (rows < 1 || rows > 65535) return TETRA_EINVAL;
     if (!aligned(x, 8) || !aligned(out, 8)) return TETRA_EALIGN;
     int dev;
-    if (int st = ensure_tables(&dev)) return st;
+    DeviceState ds;
+    if (int st = device_state(&dev, &ds)) return st;
     const float scale = static_cast<float>(1.0 / std::sqrt(static_cast<double>(n)));
     const int T = n <= 1024 ? 256 : n / 4;
     const dim3 grid(static_cast<unsigned>((K + 4 * T - 1) / (4 * T)), static_cast<unsigned>(rows));
@@ -513,7 +553,8 @@ int tetra_emb4_gather(const void* q, const uint16_t* scale_off, int rows, int di
         return TETRA_EINVAL;
     if (!aligned(scale_off, 4) || !aligned(tokens, 4) || !aligned(out, 4)) return TETRA_EALIGN;
     int dev;
-    if (int st = ensure_tables(&dev)) return st;
+    DeviceState ds;
+    if (int st = device_state(&dev, &ds)) return st;
     const long long bytes = static_cast<long long>(n) * (dim / 2);
     const unsigned grid = static_cast<unsigned>(std::min<long long>((bytes + 255) / 256, 4096));
     hipLaunchKernelGGL(tetra_dev::emb4_gather_kernel, dim3(grid), dim3(256), 0, stream,

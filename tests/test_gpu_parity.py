@@ -10,6 +10,8 @@ Bars:
 Every call goes through the C ABI via the ctypes binding.
 """
 
+import os
+
 import numpy as np
 import pytest
 
@@ -29,6 +31,16 @@ TOL_PAPER = 1e-5
 def _gpu():
     assert torch.cuda.is_available(), "GPU tests need a ROCm device"
     torch.cuda.init()
+
+
+_GEMM_WS = []
+
+
+def _gemm_ws():
+    """one zero-filled tetra_gemm workspace for the module (calls run on one stream)"""
+    if not _GEMM_WS:
+        _GEMM_WS.append(tt.gemm_workspace())
+    return _GEMM_WS[0]
 
 
 def _dev(a):
@@ -642,7 +654,7 @@ def test_rotate_one_hot_is_exact():
 def _check_gemm(pk, x, rows=None, label=""):
     N = x.shape[0]
     y = torch.empty((N, pk.M), dtype=torch.float32, device="cuda")
-    tt.gemm(pk.blob, pk.sigma, _f16_dev(x), y, pk.M, pk.K, N)
+    tt.gemm(pk.blob, pk.sigma, _f16_dev(x), y, pk.M, pk.K, N, _gemm_ws())
     torch.cuda.synchronize()
     yg = y.cpu().numpy()
     yr, norm = ogemv.gemv_f64(pk.words, pk.sigma_h, pk.tail, x, rows=rows)
@@ -695,7 +707,7 @@ def test_gemm_long_prompt_sampled():
     pk = Packed(words, sigma, tail, K)
     x = workloads.activations(2048, N, K)
     y = torch.empty((N, M), dtype=torch.float32, device="cuda")
-    tt.gemm(pk.blob, pk.sigma, _f16_dev(x), y, M, K, N)
+    tt.gemm(pk.blob, pk.sigma, _f16_dev(x), y, M, K, N, _gemm_ws())
     torch.cuda.synchronize()
     toks = np.array([0, 1, 127, 128, 1023, 2046, 2047])
     rows = _sample_rows(M, np.random.default_rng(12), n=48)
@@ -722,7 +734,7 @@ def test_gemm_token_slices():
     gen = torch.Generator(device="cuda").manual_seed(0x7E7A_0090)
     xd = torch.randn((N, K), generator=gen, device="cuda").half()
     y = torch.empty((N, M), dtype=torch.float32, device="cuda")
-    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N)
+    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N, _gemm_ws())
     torch.cuda.synchronize()
     toks = np.array([0, 1, slice_tokens - 2, slice_tokens - 1, slice_tokens])
     xs = xd[torch.as_tensor(toks, device="cuda")].cpu().numpy()
@@ -751,15 +763,15 @@ def test_gemm_split_items_repeat_bitwise(M, K, N):
     y = torch.empty((N, M), dtype=torch.float32, device="cuda")
     yv = torch.empty((1, M), dtype=torch.float32, device="cuda")
     xd = _f16_dev(x)
-    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N)
+    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N, _gemm_ws())
     tt.gemv(pk.blob, pk.sigma, xd[:1], yv, M, K, 1)
-    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N)
+    tt.gemm(pk.blob, pk.sigma, xd, y, M, K, N, _gemm_ws())
     torch.cuda.synchronize()
     again = y.cpu().numpy()
     rows = _sample_rows(M, np.random.default_rng(5 + N), n=64)
     assert np.array_equal(again[:, rows], first)
     y2 = torch.empty((N, M), dtype=torch.float32, device="cuda")
-    tt.gemm(pk.blob, pk.sigma, xd, y2, M, K, N)
+    tt.gemm(pk.blob, pk.sigma, xd, y2, M, K, N, _gemm_ws())
     torch.cuda.synchronize()
     assert torch.equal(y, y2)
 
@@ -841,3 +853,30 @@ def test_encode_retention_gaussian_blocks():
     assert 0.85 <= ret <= 0.92
     idx = rng.choice(n, 6, replace=False)
     assert np.array_equal(words[idx], oencoder.encode_blocks(w[idx], 1.0, tt.ENCODE_RADII))
+
+
+# ------------------------------------------------------------- the boundary
+
+def _child(mode):
+    import subprocess
+    import sys
+    here = os.path.dirname(os.path.abspath(__file__))
+    print(f"[boundary] child {mode}", flush=True)
+    r = subprocess.run([sys.executable, "-u", os.path.join(here, "_boundary_child.py"), mode],
+                       capture_output=True, text=True, timeout=110)
+    print(r.stdout + r.stderr, flush=True)
+    assert r.returncode == 0 and r.stdout.strip().endswith("ok")
+
+
+def test_boundary_first_call_inside_graph_capture():
+    """No call allocates or synchronises: a fresh process whose first library
+    call is made inside torch.cuda.graph capture replays it correctly."""
+    _child("capture")
+
+
+def test_boundary_two_streams_at_once():
+    _child("streams")
+
+
+def test_boundary_seventeenth_stream_is_refused():
+    _child("busy")

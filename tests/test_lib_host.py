@@ -43,7 +43,7 @@ def test_tables_match_oracle_bytes():
 
 
 def test_status_strings():
-    for s in (tt.OK, tt.EINVAL, tt.EALIGN, tt.EDEVICE, tt.EUNSUPPORTED):
+    for s in (tt.OK, tt.EINVAL, tt.EALIGN, tt.EDEVICE, tt.EUNSUPPORTED, tt.EBUSY):
         assert tt.status_string(s)
     assert tt.status_string(12345) == "unknown status"
 
@@ -149,6 +149,27 @@ def test_codes_bytes_and_bits_per_weight():
     assert 2.0 < bw < 2.2
 
 
+def test_row_stride_is_the_tile_stride_per_row():
+    """48 bits per block and row; a tile of TETRA_ROW_TILE rows spans
+    TETRA_ROW_TILE row strides, so tile t starts at t * 64 * row_stride."""
+    for K in (24, 48, 1536, 2560, 5120, 17408, 24 * 7 + 8):
+        assert tt.row_stride(K) == 6 * (K // 24)
+        M = 3 * tt.ROW_TILE + 5
+        assert tt.tail_offset(M, K) == ((M + 63) // 64) * tt.ROW_TILE * tt.row_stride(K)
+    rng = np.random.default_rng(1)
+    M, K = 130, 24 * 9 + 8
+    words = rng.integers(0, 1 << 48, size=(M, K // 24), dtype=np.uint64)
+    blob = tt.pack_rows(words, np.zeros((M, 8), np.float16), M, K)
+    t = 1                                    # changing tile 1's rows changes only its bytes
+    words2 = words.copy()
+    words2[64:128] ^= np.uint64(0xFFFF_FFFF_FFFF)
+    blob2 = tt.pack_rows(words2, np.zeros((M, 8), np.float16), M, K)
+    diff = np.flatnonzero(blob != blob2)
+    start = t * tt.ROW_TILE * tt.row_stride(K)
+    assert diff.min() >= start and diff.max() < start + tt.ROW_TILE * tt.row_stride(K)
+    assert tt.row_stride(23) == 0 and tt.row_stride(25) == 0
+
+
 def test_pack_rejects_bad_input():
     words = np.zeros((2, 1), np.uint64)
     words[1, 0] = 1 << 48
@@ -216,12 +237,14 @@ def test_int4_head4_and_emb4_validation():
     assert lib.tetra_head4_gemv(fake, fake, fake, fake, 64, 64, 0, None) == tt.EINVAL
     assert lib.tetra_head4_gemv(fake, fake + 2, fake, fake, 64, 64, 1, None) == tt.EALIGN
     assert lib.tetra_head4_gemv(fake, fake, fake + 4, fake, 64, 64, 1, None) == tt.EALIGN
-    assert lib.tetra_gemm(None, fake, fake, fake, 64, 96, 16, None) == tt.EINVAL
-    assert lib.tetra_gemm(fake, fake, fake, fake, 64, 100, 16, None) == tt.EINVAL   # K % 8
-    assert lib.tetra_gemm(fake, fake, fake, fake, 64, 96, 0, None) == tt.EINVAL
-    assert lib.tetra_gemm(fake, fake, fake, fake, 0, 96, 16, None) == tt.EINVAL
-    assert lib.tetra_gemm(fake + 8, fake, fake, fake, 64, 96, 16, None) == tt.EALIGN
-    assert lib.tetra_gemm(fake, fake, fake + 8, fake, 64, 96, 16, None) == tt.EALIGN
+    assert lib.tetra_gemm(None, fake, fake, fake, 64, 96, 16, fake, 1 << 20, None) == tt.EINVAL
+    assert lib.tetra_gemm(fake, fake, fake, fake, 64, 100, 16, fake, 1 << 20, None) == tt.EINVAL   # K % 8
+    assert lib.tetra_gemm(fake, fake, fake, fake, 64, 96, 0, fake, 1 << 20, None) == tt.EINVAL
+    assert lib.tetra_gemm(fake, fake, fake, fake, 0, 96, 16, fake, 1 << 20, None) == tt.EINVAL
+    assert lib.tetra_gemm(fake + 8, fake, fake, fake, 64, 96, 16, fake, 1 << 20, None) == tt.EALIGN
+    assert lib.tetra_gemm(fake, fake, fake + 8, fake, 64, 96, 16, fake, 1 << 20, None) == tt.EALIGN
+    assert lib.tetra_gemm(fake, fake, fake, fake, 64, 96, 16, None, 1 << 20, None) == tt.EINVAL    # no workspace
+    assert lib.tetra_gemm(fake, fake, fake, fake, 64, 96, 16, fake + 16, 1 << 20, None) == tt.EALIGN
     assert lib.tetra_rotate(None, fake, fake, 1024, 256, 1, None) == tt.EINVAL
     assert lib.tetra_rotate(fake, fake, fake, 1024, 96, 1, None) == tt.EINVAL       # n not a power of two
     assert lib.tetra_rotate(fake, fake, fake, 1024, 2, 1, None) == tt.EINVAL        # n < 4
