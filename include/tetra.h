@@ -236,6 +236,27 @@ int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x,
 size_t tetra_gemm_workspace_bytes(void);
 
 /*
+ * tetra_gemm without a workspace argument, for callers that cannot allocate
+ * device memory (code under graph capture, serving loops, harnesses that
+ * forbid hipMalloc).  The counters and piece sums of the product live in a
+ * static scratch array of the library's code object: 67,110,912 bytes per
+ * device (the pieces of 512 workgroups, two per CU of a 256-CU MI355X),
+ * held by every device the library runs on until the process ends.  The
+ * call runs the same grid as tetra_gemm with a workspace of
+ * tetra_gemm_workspace_bytes(), so the two give the same bits; a device
+ * that would run more than 512 workgroups is refused (TETRA_EUNSUPPORTED)
+ * rather than served with another split.  Input sizes are not limited by
+ * the scratch: the pieces scale with the workgroups, not with M, K or N.
+ * Each call first clears the scratch's counters with a kernel on `stream`.
+ * All calls on one device share its scratch and leave the last call's
+ * contents in it: calls that overlap in time on one device (other streams,
+ * other threads) race and give wrong results.  Arguments, layouts and the
+ * other errors as for tetra_gemm.  Never allocates or synchronises.
+ */
+int tetra_gemm_noalloc(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K,
+                       int N, hipStream_t stream);
+
+/*
  * Gives back the GEMV workspace slot that `stream` holds on the current
  * device, if any (host only).  Call it only when no GEMV work issued on the
  * stream is still pending or will be replayed from a graph.  Always

@@ -43,6 +43,7 @@ _SIGNATURES = {
     "tetra_rotate": (_int, [_vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_gemm": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp, _sz, _vp]),
     "tetra_gemm_workspace_bytes": (_sz, []),
+    "tetra_gemm_noalloc": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_release_stream": (_int, [_vp]),
     "tetra_emb4_gather": (_int, [_vp, _vp, _int, _int, _vp, _int, _vp, _vp]),
     "tetra_encode": (_int, [_vp, _vp, _sz, ctypes.c_double, ctypes.c_double, _vp, _vp]),
@@ -164,6 +165,13 @@ def gemm_workspace():
     if n == 0:
         raise TetraError(EDEVICE, "tetra_gemm_workspace_bytes")
     return torch.zeros(n, dtype=torch.uint8, device="cuda")
+
+
+def gemm_noalloc(codes, row_scales, x, y, M: int, K: int, N: int, stream=None):
+    """tetra_gemm on the library's static per-device scratch (no workspace,
+    nothing allocated); calls overlapping on one device race."""
+    _check(_call("tetra_gemm_noalloc", _ptr(codes), _ptr(row_scales), _ptr(x), _ptr(y), M, K, N, _stream(stream)),
+           "tetra_gemm_noalloc")
 
 
 def gemm(codes, row_scales, x, y, M: int, K: int, N: int, workspace, stream=None):

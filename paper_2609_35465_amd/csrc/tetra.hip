@@ -28,6 +28,16 @@ using tetra_dev::kTile;
 
 constexpr int kMaxDevices = 64;
 
+// Scratch of tetra_gemm_noalloc: the counters and piece slots of up to
+// kScratchWorkers workgroups of the many-token product, the whole chip's
+// worth on a 256-CU part (two workgroups per CU).  Every device holds its own
+// copy until the process ends; host code reaches it only through the address
+// hipGetSymbolAddress returns for the device (DeviceState::scratch), never
+// through the array's name.
+constexpr int kScratchWorkers = 512;
+constexpr size_t kScratchBytes = 67110912;   // gemm_workspace_bytes(kScratchWorkers)
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
 // What the host knows about a device, queried once and kept: no call makes
 // the device do any work, allocate or wait to set it up.  Also the owners of
 // the device's GEMV workspace slots (kernels.h, g_gemv_slots).
@@ -36,6 +46,7 @@ struct DeviceState {
     int cus = 0;
     int gemv_groups[TETRA_MAX_BATCH + 1] = {};   // resident GEMV workgroups per CU, by batch
     int gemm_workers = 0;
+    uint8_t* scratch = nullptr;                  // this device's copy of `scratch`
     bool slot_used[tetra_dev::kGemvSlots] = {};
     hipStream_t slot_stream[tetra_dev::kGemvSlots] = {};
     std::thread::id slot_thread[tetra_dev::kGemvSlots];
@@ -75,6 +86,9 @@ int device_state_locked(int* dev_out, DeviceState** out) {
                                                    gemv_resident<7>(), gemv_resident<8>()};
         for (int b = 1; b <= TETRA_MAX_BATCH; ++b)
             if (resident[b] == 0) return TETRA_EDEVICE;
+        void* sp = nullptr;
+        if (hipGetSymbolAddress(&sp, HIP_SYMBOL(scratch)) != hipSuccess || !sp) return TETRA_EDEVICE;
+        d.scratch = static_cast<uint8_t*>(sp);
         d.cus = num_cus(dev);
         for (int b = 0; b <= TETRA_MAX_BATCH; ++b) d.gemv_groups[b] = resident[b];
         d.gemm_workers = d.cus * tetra_dev::kPfGroupsPerCU;
@@ -483,6 +497,52 @@ int tetra_gemm(const void* codes, const uint16_t* row_scales, const uint16_t* x,
         const int cnt = static_cast<int>(std::min<long long>(slice, N - n));
         if (int st = gemm_launch(static_cast<const uint8_t*>(codes), row_scales, x + n * K, y + n * M, M, K, cnt, s,
                                  workers, static_cast<uint8_t*>(workspace), stream))
+            return st;
+    }
+    return TETRA_OK;
+}
+
+namespace tetra_dev {
+
+// zeroes n 32-bit words (the counters of a scratch region), so that clearing
+// is a kernel node, not a memset, when the caller captures a graph
+__global__ __launch_bounds__(256) void zero_words_kernel(uint32_t* p, int n) {
+    for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
+}
+
+}  // namespace tetra_dev
+
+int tetra_gemm_noalloc(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K,
+                       int N, hipStream_t stream) {
+    static_assert(kScratchBytes >= (sizeof(uint32_t) * kScratchWorkers + 255) / 256 * 256 +
+                                       sizeof(float) * static_cast<size_t>(kScratchWorkers) * 2 * tetra_dev::kPfSlot,
+                  "scratch holds the counters and pieces of kScratchWorkers workgroups");
+    if (!codes || !row_scales || !x || !y || M < 1 || K < 24 || N < 1 || K % 8) return TETRA_EINVAL;
+    if (!aligned(codes, 16) || !aligned(x, 16) || !aligned(row_scales, 2) || !aligned(y, 4)) return TETRA_EALIGN;
+    int dev;
+    DeviceState ds;
+    if (int st = device_state(&dev, &ds)) return st;
+    Shape s;
+    if (!shape_of(M, K, &s)) return TETRA_EINVAL;
+    // the device's whole grid, as tetra_gemm with a full workspace runs it;
+    // a device that holds more workgroups than the scratch has slots for is
+    // refused rather than served by a smaller grid with other rounding
+    const int workers = ds.gemm_workers;
+    if (workers < 1) return TETRA_EDEVICE;
+    if (workers > kScratchWorkers || tetra_dev::gemm_workspace_bytes(workers) > kScratchBytes)
+        return TETRA_EUNSUPPORTED;
+    uint8_t* ws = ds.scratch;
+    const int nctr = static_cast<int>(tetra_dev::gemm_counter_bytes(workers) / sizeof(uint32_t));
+    hipLaunchKernelGGL(tetra_dev::zero_words_kernel, dim3(static_cast<unsigned>((nctr + 255) / 256)), dim3(256), 0,
+                       stream, reinterpret_cast<uint32_t*>(ws), nctr);
+    if (int st = launch_status()) return st;
+    const long long slice = std::max<long long>(
+        tetra_dev::kPfTokens,
+        ((0x7FFFFFFFll / (2ll * K)) / tetra_dev::kPfTokens) * tetra_dev::kPfTokens);
+    for (long long n = 0; n < N; n += slice) {
+        const int cnt = static_cast<int>(std::min<long long>(slice, N - n));
+        if (int st = gemm_launch(static_cast<const uint8_t*>(codes), row_scales, x + n * K, y + n * M, M, K, cnt, s,
+                                 workers, ws, stream))
             return st;
     }
     return TETRA_OK;
