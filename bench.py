@@ -48,7 +48,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--mode", default="deps", choices=["matrix", "deps", "layer"],
+    ap.add_argument("--chain-layers", type=int, default=1,
+                    help="--mode chain: layers per launch (1 or 2)")
+    ap.add_argument("--mode", default="deps", choices=["matrix", "deps", "layer", "chain"],
                     help="matrix: one launch per matrix; deps: per layer [q,k,v] [o] "
                          "[gate,up] [down] (the launches a decode step can fuse); "
                          "layer: one grouped launch per layer")
@@ -151,12 +153,49 @@ GROUPS = {
 }
 
 
-def build_launches(tt, plan, mode, nproj=7, emb=None):
+def build_chains(tt, plan, chain_layers, nproj=7):
+    """Launches of one step as chains: the dependency groups of chain_layers
+    layers are the phases of one tetra_gemv_chain launch; a group with int4
+    members ends its chain (its Tetra members are the chain's last phase) and
+    its int4 members run next, so the order of the groups is kept."""
+    launches = []
+    cur, counts, mats = [], [], []
+
+    def flush():
+        if counts:
+            launches.append(("chain", tt.make_problems(cur), list(counts), list(mats)))
+        cur.clear(), counts.clear(), mats.clear()
+
+    for l0 in range(0, len(plan), nproj):
+        if (l0 // nproj) % chain_layers == 0:
+            flush()
+        layer = plan[l0:l0 + nproj]
+        by_name = {m.name: (m, x, y) for m, x, y in layer}
+        for names in GROUPS["deps"]:
+            tet = [n for n in names if isinstance(by_name[n][0], Matrix)]
+            i4 = [n for n in names if not isinstance(by_name[n][0], Matrix)]
+            if tet:
+                cur.extend((by_name[n][0].blob, by_name[n][0].sigma, by_name[n][1], by_name[n][2],
+                            by_name[n][0].M, by_name[n][0].K) for n in tet)
+                counts.append(len(tet))
+                mats.extend(by_name[n][0] for n in tet)
+            if i4:
+                flush()
+                for n in i4:
+                    launches.append(("int4",) + by_name[n])
+    flush()
+    return launches
+
+
+def build_launches(tt, plan, mode, nproj=7, emb=None, chain_layers=1):
     """Launches of one step, in order: ("tetra", problem array, matrices),
-    ("int4", matrix, x, y) or ("emb4", table)."""
+    ("chain", problem array, phase counts, matrices), ("int4", matrix, x, y)
+    or ("emb4", table)."""
     launches = []
     if emb is not None:
         launches.append(("emb4", emb))
+    if mode == "chain":
+        return launches + build_chains(tt, plan, chain_layers, nproj)
     for l0 in range(0, len(plan), nproj):
         layer = plan[l0:l0 + nproj]
         by_name = {m.name: (m, x, y) for m, x, y in layer}
@@ -176,6 +215,8 @@ def run_step(tt, launches, batch, stream, only_tetra=False):
     for ln in launches:
         if ln[0] == "tetra":
             tt.gemv_grouped(ln[1], batch, stream)
+        elif ln[0] == "chain":
+            tt.gemv_chain(ln[1], ln[2], batch, None, stream)
         elif only_tetra:
             continue
         elif ln[0] == "int4":
@@ -691,8 +732,8 @@ def main():
     algo_bytes = bytes_read + bytes_xy
     tetra_bytes = sum(m.read_bytes + 2 * m.K * args.batch + 4 * m.M * args.batch for m, _, _ in tetra)
 
-    launches = build_launches(tt, plan, args.mode, emb=emb)
-    n_tetra = sum(1 for ln in launches if ln[0] == "tetra")
+    launches = build_launches(tt, plan, args.mode, emb=emb, chain_layers=args.chain_layers)
+    n_tetra = sum(1 for ln in launches if ln[0] in ("tetra", "chain"))
     # warm-up (also uploads the decoder tables and sets up the workspace)
     for _ in range(max(1, args.warmup)):
         run_step(tt, launches, args.batch, stream.cuda_stream)
@@ -774,7 +815,9 @@ def main():
             "batch": args.batch, "layers": L, "matrices": len(plan), "tetra_matrices": len(tetra),
             "hip_graph": graph is not None, "launches_per_step": len(launches),
             "launch_grouping": args.mode,
-        },
+        } | ({"chain_layers": args.chain_layers,
+              "phases_per_step": sum(len(ln[2]) for ln in launches if ln[0] == "chain")}
+             if args.mode == "chain" else {}),
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "bits_read_per_weight": round(bits_w, 4),
         "weights_per_s": round(weights / (ms_step * 1e-3), 1),

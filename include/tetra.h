@@ -56,7 +56,8 @@ typedef enum {
     TETRA_EALIGN = -2,       /* a device pointer is not aligned as required */
     TETRA_EDEVICE = -3,      /* HIP runtime error (device query or launch)  */
     TETRA_EUNSUPPORTED = -4, /* valid request the library does not serve    */
-    TETRA_EBUSY = -5         /* all GEMV workspace slots held by other streams */
+    TETRA_EBUSY = -5,        /* all GEMV workspace slots held by other streams */
+    TETRA_ETIMEOUT = -6      /* a wait between the phases of tetra_gemv_chain gave up */
 } tetra_status;
 
 /* Rows of one code tile of the device layout (see tetra_pack_rows). */
@@ -190,6 +191,49 @@ typedef struct {
  */
 int tetra_gemv_grouped(const tetra_gemv_problem* problems, int n, int batch,
                        hipStream_t stream);
+
+/* Largest number of phases in one tetra_gemv_chain call. */
+#define TETRA_MAX_PHASES 16
+
+/*
+ * Several groups of Tetra products run in order in one launch: the
+ * dependency groups of a decode step (Sec. 5.1, Sec. 6: the q, k, v
+ * projections, then o, then gate and up, then down) without a kernel
+ * boundary between them.  Phase k holds phase_counts[k] problems; the
+ * problems are listed in phase order (n = sum of the counts, 1..
+ * TETRA_MAX_GROUP in all; n_phases 1..TETRA_MAX_PHASES).  Every product is
+ * computed exactly as tetra_gemv computes it, with the same bits as a
+ * tetra_gemv_grouped call of its phase on a device where both run the
+ * same number of waves.  The launch holds every workgroup the device keeps
+ * resident at once; the decoder tables are staged once, and no workgroup
+ * starts the products of phase k + 1 before every workgroup has finished
+ * phase k (a device-wide barrier; only the code words of phase k + 1, which
+ * no phase writes, are requested before it).  The barrier orders execution,
+ * not memory: the inputs of a phase must not be outputs of an earlier phase
+ * of the same call.
+ *   problems:     host array, read during the call only
+ *   phase_counts: host array of n_phases counts >= 1
+ *   status:       device int, 4-byte aligned, or NULL: when the launch
+ *                 ends it holds 0, or TETRA_ETIMEOUT if a wait between
+ *                 phases gave up.  Each wait is bounded (see
+ *                 tetra_set_chain_wait_limit), so a launch whose workgroups
+ *                 cannot all be resident at once still ends; a workgroup
+ *                 whose wait gives up abandons the rest of the launch, and
+ *                 the outputs of its phases are then undefined.  The
+ *                 workspace slot is left ready for the next call either way.
+ * Asynchronous; status codes as for tetra_gemv_grouped, checked before any
+ * launch.  Shares the stream's workspace slot with tetra_gemv.
+ */
+int tetra_gemv_chain(const tetra_gemv_problem* problems, int n, const int* phase_counts, int n_phases,
+                     int batch, int* status, hipStream_t stream);
+
+/*
+ * Test hook: the number of polls (about a microsecond each) after which a
+ * wait of later tetra_gemv_chain launches gives up; 0 restores the default
+ * (2^20).  Returns the previous value.  Host only; affects launches made
+ * after it returns.
+ */
+uint32_t tetra_set_chain_wait_limit(uint32_t polls);
 
 /*
  * Bulk decode of n canonical words (Sec. 3.4, Fig. 4), for testing.

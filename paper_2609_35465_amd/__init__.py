@@ -15,7 +15,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtetra.so")
 
-OK, EINVAL, EALIGN, EDEVICE, EUNSUPPORTED, EBUSY = 0, -1, -2, -3, -4, -5
+OK, EINVAL, EALIGN, EDEVICE, EUNSUPPORTED, EBUSY, ETIMEOUT = 0, -1, -2, -3, -4, -5, -6
 ROW_TILE = 64
 TABLE_BLOB_BYTES = 18824
 MAX_BATCH = 8
@@ -36,6 +36,8 @@ _SIGNATURES = {
     "tetra_unpack_rows": (_int, [_vp, _sz, _int, _int, _vp, _vp]),
     "tetra_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
     "tetra_gemv_grouped": (_int, [_vp, _int, _int, _vp]),
+    "tetra_gemv_chain": (_int, [_vp, _int, _vp, _int, _int, _vp, _vp]),
+    "tetra_set_chain_wait_limit": (ctypes.c_uint32, [ctypes.c_uint32]),
     "tetra_decode": (_int, [_vp, _sz, _vp, _vp, _vp]),
     "tetra_dequant": (_int, [_vp, _vp, _int, _int, _vp, _vp]),
     "tetra_int4_gemv": (_int, [_vp, _vp, _vp, _vp, _int, _int, _int, _vp]),
@@ -215,6 +217,21 @@ def gemv_grouped(problems, batch: int = 1, stream=None):
     """Several products in one launch; problems from make_problems()."""
     _check(_call("tetra_gemv_grouped", ctypes.cast(problems, ctypes.c_void_p), len(problems),
                  batch, _stream(stream)), "tetra_gemv_grouped")
+
+
+def gemv_chain(problems, phase_counts, batch: int = 1, status=None, stream=None):
+    """Phases of products in order in one launch (problems from
+    make_problems(), in phase order; phase k holds phase_counts[k] of them);
+    status: an optional device int32 tensor that receives the launch's status."""
+    counts = (ctypes.c_int * len(phase_counts))(*[int(c) for c in phase_counts])
+    _check(_call("tetra_gemv_chain", ctypes.cast(problems, ctypes.c_void_p), len(problems),
+                 ctypes.cast(counts, ctypes.c_void_p), len(phase_counts), batch, _ptr(status), _stream(stream)),
+           "tetra_gemv_chain")
+
+
+def set_chain_wait_limit(polls: int) -> int:
+    """Test hook: polls before a chain barrier wait gives up (0: default)."""
+    return int(_call("tetra_set_chain_wait_limit", int(polls)))
 
 
 def decode(words_bytes, n: int, y_out, scale_out=None, stream=None):

@@ -289,12 +289,29 @@ struct GemvProblem {
     int tiles, ng, rem;
 };
 
-struct GemvGroup {
-    GemvProblem prob[kMaxGroup];
+// The even split of one phase's block sequence (its problems, matrix by
+// matrix, tile by tile, block column by block column) over its waves.
+struct GemvSplit {
     double inv_total, inv_waves;   // 1 / total, 1 / waves
-    uint32_t total;                // blocks in the launch sequence (< 2^31)
-    int slot;                      // workspace slot of the launch (g_gemv_slots)
-    int n, waves;
+    uint32_t total;                // blocks in the phase (< 2^31)
+    int waves;                     // waves that take a range (the launch's first `waves`)
+    int p0, n;                     // its problems: prob[p0 .. p0 + n - 1]
+};
+
+constexpr int kMaxPhases = 16;
+constexpr int kChainTimeout = -6;   // TETRA_ETIMEOUT
+
+// One launch: phases run in order, each split over the launch's waves; a
+// wave starts phase k + 1 only after every workgroup of the launch has
+// finished phase k (the chain barrier below).  A single-phase launch is a
+// plain (grouped) product.
+struct GemvChain {
+    GemvProblem prob[kMaxGroup];   // blk_base counts from the start of the problem's phase
+    GemvSplit ph[kMaxPhases];
+    int n_phases;
+    int slot;                      // workspace slot of the launch (g_gemv_slots, g_chain_sync)
+    uint32_t wait_limit;           // polls before a chain barrier wait gives up
+    int* status;                   // device word for the launch's status, or null
 };
 
 // GEMV workspaces: a counter and two partial sums per workgroup.  One slot
@@ -315,18 +332,79 @@ struct GemvSlot {
 
 __device__ GemvSlot g_gemv_slots[kGemvSlots];
 
-// wave count of a launch: one round of the 768-thread workgroups a CU holds
-// at once (`groups`: two at batch 1 and 2; one from batch 3 on, whose
-// registers allow 12 waves per CU), fewer when the launch is small, so that
-// each wave takes at least kGemvMinBlocks blocks (a wave's fixed cost, table
-// staging and its share of the piece reduction, is worth several blocks of
-// streaming; every range is non-empty).  A second round of workgroups would
-// pay the launch start and the piece reduction twice.
+// Words of the chain barrier of a slot, each on its own 128-byte line.  The
+// workgroups of a launch form eight groups (blockIdx mod 8); a workgroup done
+// with phase k counts itself into its group, the last of a group counts the
+// group into `count`, and the last group raises every group's flag to k + 1,
+// which the group's workgroups poll.  Spreading the arrivals over eight
+// counters keeps them from queueing on one address (measured: 2.2 us per
+// barrier for 512 workgroups, against 8.3 us with one counter).  All words
+// are touched only with device-scope atomics.  Counts and flags grow within
+// a launch; the last workgroup to finish the launch puts them back to zero.
+struct ChainSync {
+    uint32_t grp[8][32];
+    uint32_t count[32];
+    uint32_t flag[8][32];
+    uint32_t exit[32];             // workgroups finished
+    uint32_t expired[32];          // waits that gave up
+};
+
+__device__ ChainSync g_chain_sync[kGemvSlots];
+
+__device__ __forceinline__ uint32_t dev_load(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t dev_add(uint32_t* p, uint32_t v) {
+    return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void dev_store(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// workgroup `wg` of `nwg` is done with phase k (one thread per workgroup)
+__device__ __forceinline__ void chain_arrive(ChainSync& cs, int k, int wg, int nwg) {
+    const uint32_t q = static_cast<uint32_t>(wg) & 7u;
+    const uint32_t groups = nwg < 8 ? static_cast<uint32_t>(nwg) : 8u;
+    const uint32_t per = static_cast<uint32_t>(nwg) / 8u + ((static_cast<uint32_t>(nwg) & 7u) > q ? 1u : 0u);
+    const uint32_t target = static_cast<uint32_t>(k) + 1u;
+    if (dev_add(&cs.grp[q][0], 1u) + 1u == target * per)
+        if (dev_add(&cs.count[0], 1u) + 1u == target * groups)
+            for (uint32_t h = 0; h < groups; ++h) dev_store(&cs.flag[h][0], target);
+}
+
+// waits until every workgroup is done with phase k; false when it gave up
+// after `limit` polls
+__device__ __forceinline__ bool chain_wait(const ChainSync& cs, int k, int wg, uint32_t limit) {
+    const uint32_t q = static_cast<uint32_t>(wg) & 7u;
+    const uint32_t target = static_cast<uint32_t>(k) + 1u;
+    for (uint32_t n = 0; dev_load(&cs.flag[q][0]) < target;) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++n > limit) return false;
+    }
+    return true;
+}
+
+// wave count of a single-phase launch: one round of the 768-thread
+// workgroups a CU holds at once (`groups`: two at batch 1 and 2; one from
+// batch 3 on, whose registers allow 12 waves per CU), fewer when the launch
+// is small, so that each wave takes at least kGemvMinBlocks blocks (a wave's
+// fixed cost, table staging and its share of the piece reduction, is worth
+// several blocks of streaming; every range is non-empty).  A second round of
+// workgroups would pay the launch start and the piece reduction twice.
 constexpr uint32_t kGemvMinBlocks = 8;
 inline int gemv_waves(uint32_t total, int cus, int groups) {
     const uint32_t cap = static_cast<uint32_t>(cus) * static_cast<uint32_t>(groups) * kGemvWaves;
     const uint32_t want = total / kGemvMinBlocks > 0 ? total / kGemvMinBlocks : 1u;
     return static_cast<int>(want < cap ? want : cap);
+}
+
+// Waves of one phase of a chain: its launch holds a whole round of
+// workgroups anyway, and the tables are staged once for all phases, so a
+// wave is worth fewer blocks than in a single launch.
+constexpr uint32_t kChainMinBlocks = 4;
+inline int chain_phase_waves(uint32_t total, int launch_waves) {
+    const uint32_t want = total / kChainMinBlocks > 0 ? total / kChainMinBlocks : 1u;
+    return static_cast<int>(want < static_cast<uint32_t>(launch_waves) ? want : static_cast<uint32_t>(launch_waves));
 }
 
 // largest workgroup count of a launch at batch B that the slot's partial
@@ -345,15 +423,15 @@ __device__ __forceinline__ uint32_t div_exact(unsigned long long n, uint32_t d, 
     return q;
 }
 
-__device__ __forceinline__ uint32_t range_begin(int w, const GemvGroup& grp) {
-    return div_exact(static_cast<unsigned long long>(grp.total) * static_cast<uint32_t>(w),
-                     static_cast<uint32_t>(grp.waves), grp.inv_waves);
+__device__ __forceinline__ uint32_t range_begin(int w, const GemvSplit& sp) {
+    return div_exact(static_cast<unsigned long long>(sp.total) * static_cast<uint32_t>(w),
+                     static_cast<uint32_t>(sp.waves), sp.inv_waves);
 }
 
 // the wave whose range holds block i: floor(((i + 1) W - 1) / total)
-__device__ __forceinline__ int wave_of(uint32_t i, const GemvGroup& grp) {
-    return static_cast<int>(div_exact(static_cast<unsigned long long>(i + 1) * static_cast<uint32_t>(grp.waves) - 1,
-                                      grp.total, grp.inv_total));
+__device__ __forceinline__ int wave_of(uint32_t i, const GemvSplit& sp) {
+    return static_cast<int>(div_exact(static_cast<unsigned long long>(i + 1) * static_cast<uint32_t>(sp.waves) - 1,
+                                      sp.total, sp.inv_total));
 }
 
 // code words of one item (a group of four block columns, or the nblk mod 4
@@ -977,160 +1055,251 @@ __device__ __forceinline__ void store_rows(const GemvProblem& P, int t, const fl
     }
 }
 
+// Where a wave's range of a phase starts: problem p (absolute index), tile
+// t, columns c..c1-1 of its first piece, blocks i..end-1 of the phase's
+// sequence; live is false for a wave past the phase's waves.
+struct RangePos {
+    int p, t, c, c1;
+    uint32_t i, end;
+    bool live;
+};
+
+__device__ __forceinline__ RangePos range_pos(const GemvChain& ch, int k, int w) {
+    const GemvSplit& sp = ch.ph[k];
+    RangePos r;
+    r.live = w < sp.waves;
+    const int wr = r.live ? w : sp.waves - 1;
+    r.i = __builtin_amdgcn_readfirstlane(range_begin(wr, sp));
+    r.end = __builtin_amdgcn_readfirstlane(range_begin(wr + 1, sp));
+    int p = sp.p0;
+    while (p + 1 < sp.p0 + sp.n && r.i >= ch.prob[p + 1].blk_base) ++p;
+    r.p = p;
+    const GemvProblem& P = ch.prob[p];
+    const uint32_t rel = r.i - P.blk_base;
+    r.t = __builtin_amdgcn_readfirstlane(static_cast<int>(rel / static_cast<uint32_t>(P.nblk)));
+    r.c = __builtin_amdgcn_readfirstlane(static_cast<int>(rel - static_cast<uint32_t>(r.t) * P.nblk));
+    const uint32_t left = r.end - r.i;
+    r.c1 = left < static_cast<uint32_t>(P.nblk - r.c) ? r.c + static_cast<int>(left) : P.nblk;
+    return r;
+}
+
 // Pieces of a tile are combined in two levels: the waves of one workgroup
 // that hold pieces of the tile add them in LDS (the last of them to arrive,
 // in wave order), and when the tile reaches into other workgroups each
 // workgroup's sum goes to the workspace, where the last workgroup to arrive
-// adds them in workgroup order.
+// adds them in workgroup order.  Piece p of a wave's range: its sum, then
+// its share of the tile's reduction.
 template <int B>
+__device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSplit& sp, int t, int c, int c1,
+                                             bool first, const float (&sum)[B], int w0, int g, float* s_piece,
+                                             uint32_t* s_cnt, uint32_t* counters, float* partials) {
+    if (c == 0 && c1 == P.nblk) {
+        const RowTail rt = load_rows(P, t);
+        store_rows<B>(P, t, sum, rt);
+        return;
+    }
+    const int wid = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    const int wlast = min(w0 + kGemvWaves, sp.waves) - 1;
+    const uint32_t t0 = P.blk_base + static_cast<uint32_t>(t) * P.nblk;
+    const int wa = __builtin_amdgcn_readfirstlane(wave_of(t0, sp));
+    const int wb = __builtin_amdgcn_readfirstlane(wave_of(t0 + P.nblk - 1, sp));
+    // slot of wave v's piece of this tile: 0 when the tile is where v's range
+    // starts, which holds for every contributor but possibly the first
+    const int slot_wa = __builtin_amdgcn_readfirstlane(range_begin(wa, sp) >= t0 ? 0 : 1);
+    auto slot_of = [&](int v) { return v > wa ? 0 : slot_wa; };
+    const int a = max(wa, w0), b = min(wb, wlast);
+    const int ln = lane_now();
+    float* mine = s_piece + (wid * 2 + (first ? 0 : 1)) * B * 64 + ln;
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) mine[bb * 64] = sum[bb];
+    // LDS operations of a wave complete in order, and the last wave reads the
+    // pieces only after its own count: no fence is needed
+    uint32_t arrived = 0;
+    if (ln == 0)
+        arrived = __hip_atomic_fetch_add(s_cnt + 2 * (b - w0) + slot_of(b), 1u, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_WORKGROUP);
+    arrived = __builtin_amdgcn_readfirstlane(arrived);
+    if (arrived != static_cast<uint32_t>(b - a)) return;
+    // last of this workgroup's pieces of the tile: add them in wave order
+    const RowTail rt = load_rows(P, t);   // in flight while the sums combine
+    float tot[B];
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
+    for (int v = a; v <= b; ++v) {
+        const float* pv = s_piece + ((v - w0) * 2 + slot_of(v)) * B * 64 + ln;
+#pragma unroll
+        for (int bb = 0; bb < B; ++bb) tot[bb] += pv[bb * 64];
+    }
+    if (wa >= w0 && wb <= wlast) {
+        store_rows<B>(P, t, tot, rt);
+        return;
+    }
+    // the tile reaches into other workgroups: publish this workgroup's sum.
+    // Workgroup sums and counters are accessed only with device-scope
+    // atomics, which are coherent across the chip's L2 caches; the wait
+    // orders the sum before the count.
+    const int ga = wa / kGemvWaves, gb = wb / kGemvWaves;
+    const int gslot_ga = __builtin_amdgcn_readfirstlane(range_begin(ga * kGemvWaves, sp) >= t0 ? 0 : 1);
+    auto gslot_of = [&](int h) { return h > ga ? 0 : gslot_ga; };
+    float* gp = partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + ln;
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb)
+        __hip_atomic_store(gp + bb * 64, tot[bb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    uint32_t garr = 0;
+    if (ln == 0) garr = __hip_atomic_fetch_add(counters + gb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    garr = __builtin_amdgcn_readfirstlane(garr);
+    if (garr != static_cast<uint32_t>(gb - ga)) return;
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
+    // loads in batches of eight, added in workgroup order
+    for (int h0 = ga; h0 <= gb; h0 += 8) {
+        float pv[8][B];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int h = h0 + u;
+            if (h <= gb) {
+                const float* ph = partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + ln;
+#pragma unroll
+                for (int bb = 0; bb < B; ++bb)
+                    pv[u][bb] = __hip_atomic_load(ph + bb * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (h0 + u <= gb) {
+#pragma unroll
+                for (int bb = 0; bb < B; ++bb) tot[bb] += pv[u][bb];
+            }
+    }
+    if (ln == 0) __hip_atomic_store(counters + gb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    store_rows<B>(P, t, tot, rt);
+}
+
+// The whole launch: decoder tables staged once, then the phases in order (one
+// for a plain or grouped product, Chain false).  A wave walks the pieces of
+// its range of a phase; at the range's end (Chain) it requests the code words
+// of its first piece of the next phase, which no phase writes, and its
+// workgroup waits at the chain barrier with those words in flight.  A wave
+// with no range in a phase goes straight to the barrier.
+template <int B, bool Chain>
 __global__ __launch_bounds__(kGemvThreads) __attribute__((amdgpu_waves_per_eu(B <= 2 ? 6 : 3)))
-void gemv_kernel(const GemvGroup grp) {
+void gemv_kernel(const GemvChain ch) {
     __shared__ uint4 s_tab[kPackedTableBytes / 16];
     __shared__ float s_piece[kGemvWaves * 2 * B * 64];   // [wave][first/last piece][B][64]
-    __shared__ uint32_t s_cnt[2 * kGemvWaves];
+    __shared__ uint32_t s_cnt[2 * kGemvWaves + 1];       // piece counts; the last word: the launch is abandoned
     constexpr bool kMx = B >= 3;
     __shared__ uint4 s_xs[kMx ? kGemvWaves * MxSets<B>::kN * kXSlotBytes / 16 : 1];   // batch >= 3: x slots per wave
     if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
     lds_bytes* L = (lds_bytes*)(s_tab);
     const int lane = threadIdx.x & 63;
-    const int W = grp.waves;
     const int wid = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
     const int g = static_cast<int>(blockIdx.x);
     const int w0 = g * kGemvWaves;
     const int w = w0 + wid;
-    const int wlast = min(w0 + kGemvWaves, W) - 1;
     TableStage<kGemvThreads> ts;
     ts.load();
-    uint32_t i = __builtin_amdgcn_readfirstlane(range_begin(w, grp));
-    const uint32_t end = __builtin_amdgcn_readfirstlane(range_begin(w + 1, grp));
-    uint32_t* const counters = g_gemv_slots[grp.slot].counters;
-    float* const partials = g_gemv_slots[grp.slot].partials;
-    int p = 0;
-    while (p + 1 < grp.n && i >= grp.prob[p + 1].blk_base) ++p;
-    const uint32_t rel = i - grp.prob[p].blk_base;
-    int t = __builtin_amdgcn_readfirstlane(static_cast<int>(rel / static_cast<uint32_t>(grp.prob[p].nblk)));
-    int c = __builtin_amdgcn_readfirstlane(static_cast<int>(rel - static_cast<uint32_t>(t) * grp.prob[p].nblk));
-    int c1;
-    {
-        const uint32_t left = end - i;
-        c1 = left < static_cast<uint32_t>(grp.prob[p].nblk - c) ? c + static_cast<int>(left) : grp.prob[p].nblk;
-    }
+    uint32_t* const counters = g_gemv_slots[ch.slot].counters;
+    float* const partials = g_gemv_slots[ch.slot].partials;
     // the first piece's code words are requested while the tables arrive;
     // the barrier orders LDS only, so they stay in flight across it
-    Piece pc = begin_piece_live(grp.prob[p], t, c, c1, lane, w < W);
+    RangePos r = range_pos(ch, 0, w);
+    int p = r.p, t = r.t, c = r.c, c1 = r.c1;
+    uint32_t i = r.i, end = r.end;
+    Piece pc = begin_piece_live(ch.prob[p], t, c, c1, lane, r.live);
     XGroup<B> xp;
-    if constexpr (kMx) xp = begin_xpiece<B>(grp.prob[p], pc, w < W);
+    if constexpr (kMx) xp = begin_xpiece<B>(ch.prob[p], pc, r.live);
     uint8_t* xs = reinterpret_cast<uint8_t*>(s_xs) + (kMx ? wid * MxSets<B>::kN * kXSlotBytes : 0);
     ts.store(s_tab);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-    if (w >= W) return;
+    if constexpr (!Chain) {
+        if (!r.live) return;
+    }
+    int k = 0;                    // the phase
+    bool live = r.live;
     bool first = true;
     for (;;) {
-        const GemvProblem& P = grp.prob[p];
-        float sum[B];
-        if constexpr (kMx) run_piece_mx<B>(P, pc, xp, L, xs, sum);
-        else run_piece<B>(P, pc, L, sum);
-        if (c == 0 && c1 == P.nblk) {
-            const RowTail rt = load_rows(P, t);
-            store_rows<B>(P, t, sum, rt);
-        } else {
-            const uint32_t t0 = P.blk_base + static_cast<uint32_t>(t) * P.nblk;
-            const int wa = __builtin_amdgcn_readfirstlane(wave_of(t0, grp));
-            const int wb = __builtin_amdgcn_readfirstlane(wave_of(t0 + P.nblk - 1, grp));
-            // slot of wave v's piece of this tile: 0 when the tile is where v's range
-            // starts, which holds for every contributor but possibly the first
-            const int slot_wa = __builtin_amdgcn_readfirstlane(range_begin(wa, grp) >= t0 ? 0 : 1);
-            auto slot_of = [&](int v) { return v > wa ? 0 : slot_wa; };
-            const int a = max(wa, w0), b = min(wb, wlast);
-            const int ln = lane_now();
-            float* mine = s_piece + (wid * 2 + (first ? 0 : 1)) * B * 64 + ln;
-#pragma unroll
-            for (int bb = 0; bb < B; ++bb) mine[bb * 64] = sum[bb];
-            // LDS operations of a wave complete in order, and the last wave reads the
-            // pieces only after its own count: no fence is needed
-            uint32_t arrived = 0;
-            if (ln == 0)
-                arrived = __hip_atomic_fetch_add(s_cnt + 2 * (b - w0) + slot_of(b), 1u, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_WORKGROUP);
-            arrived = __builtin_amdgcn_readfirstlane(arrived);
-            if (arrived == static_cast<uint32_t>(b - a)) {
-                // last of this workgroup's pieces of the tile: add them in wave order
-                const RowTail rt = load_rows(P, t);   // in flight while the sums combine
-                float tot[B];
-#pragma unroll
-                for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
-                for (int v = a; v <= b; ++v) {
-                    const float* pv = s_piece + ((v - w0) * 2 + slot_of(v)) * B * 64 + ln;
-#pragma unroll
-                    for (int bb = 0; bb < B; ++bb) tot[bb] += pv[bb * 64];
+        if (!Chain || live) {
+            const GemvProblem& P = ch.prob[p];
+            float sum[B];
+            if constexpr (kMx) run_piece_mx<B>(P, pc, xp, L, xs, sum);
+            else run_piece<B>(P, pc, L, sum);
+            finish_piece<B>(P, ch.ph[k], t, c, c1, first, sum, w0, g, s_piece, s_cnt, counters, partials);
+            i += static_cast<uint32_t>(c1 - c);
+            if (i < end) {
+                first = false;
+                c = 0;
+                if (++t == ch.prob[p].tiles) {
+                    t = 0;
+                    ++p;
                 }
-                if (wa >= w0 && wb <= wlast) {
-                    store_rows<B>(P, t, tot, rt);
-                } else {
-                    // the tile reaches into other workgroups: publish this workgroup's sum.
-                    // Workgroup sums and counters are accessed only with device-scope
-                    // atomics, which are coherent across the chip's L2 caches; the wait
-                    // orders the sum before the count.
-                    const int ga = wa / kGemvWaves, gb = wb / kGemvWaves;
-                    const int gslot_ga =
-                        __builtin_amdgcn_readfirstlane(range_begin(ga * kGemvWaves, grp) >= t0 ? 0 : 1);
-                    auto gslot_of = [&](int h) { return h > ga ? 0 : gslot_ga; };
-                    float* gp = partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + ln;
-#pragma unroll
-                    for (int bb = 0; bb < B; ++bb)
-                        __hip_atomic_store(gp + bb * 64, tot[bb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-                    uint32_t garr = 0;
-                    if (ln == 0)
-                        garr = __hip_atomic_fetch_add(counters + gb, 1u, __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT);
-                    garr = __builtin_amdgcn_readfirstlane(garr);
-                    if (garr == static_cast<uint32_t>(gb - ga)) {
-#pragma unroll
-                        for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
-                        // loads in batches of eight, added in workgroup order
-                        for (int h0 = ga; h0 <= gb; h0 += 8) {
-                            float pv[8][B];
-#pragma unroll
-                            for (int u = 0; u < 8; ++u) {
-                                const int h = h0 + u;
-                                if (h <= gb) {
-                                    const float* ph =
-                                        partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + ln;
-#pragma unroll
-                                    for (int bb = 0; bb < B; ++bb)
-                                        pv[u][bb] = __hip_atomic_load(ph + bb * 64, __ATOMIC_RELAXED,
-                                                                      __HIP_MEMORY_SCOPE_AGENT);
-                                }
-                            }
-#pragma unroll
-                            for (int u = 0; u < 8; ++u)
-                                if (h0 + u <= gb) {
-#pragma unroll
-                                    for (int bb = 0; bb < B; ++bb) tot[bb] += pv[u][bb];
-                                }
-                        }
-                        if (ln == 0)
-                            __hip_atomic_store(counters + gb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        store_rows<B>(P, t, tot, rt);
-                    }
-                }
+                const uint32_t left = end - i;
+                c1 = left < static_cast<uint32_t>(ch.prob[p].nblk) ? static_cast<int>(left) : ch.prob[p].nblk;
+                pc = begin_piece(ch.prob[p], t, 0, c1, lane);
+                if constexpr (kMx) xp = begin_xpiece<B>(ch.prob[p], pc, true);
+                continue;
             }
         }
-        i += static_cast<uint32_t>(c1 - c);
-        if (i >= end) break;
-        first = false;
-        c = 0;
-        if (++t == grp.prob[p].tiles) {
-            t = 0;
-            ++p;
+        if constexpr (!Chain) {
+            break;
+        } else {
+            // the wave's range of phase k is done
+            if (++k == ch.n_phases) break;
+            r = range_pos(ch, k, w);
+            p = r.p;
+            t = r.t;
+            c = r.c;
+            c1 = r.c1;
+            i = r.i;
+            end = r.end;
+            live = r.live;
+            first = true;
+            pc = begin_piece_live(ch.prob[p], t, c, c1, lane, live);
+            if constexpr (kMx) xp = begin_xpiece<B>(ch.prob[p], pc, live);
+            // every wave of the workgroup is done with phase k - 1 (and with its
+            // LDS pieces and counts); one lane counts the workgroup in and waits
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+            if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
+            if (threadIdx.x == 0) {
+                ChainSync& cs = g_chain_sync[ch.slot];
+                chain_arrive(cs, k - 1, g, static_cast<int>(gridDim.x));
+                const bool met = chain_wait(cs, k - 1, g, ch.wait_limit);
+                if (!met) dev_add(&cs.expired[0], 1u);
+                s_cnt[2 * kGemvWaves] = met ? 0u : 1u;
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+            // a wait that gave up abandons the launch: running ahead could
+            // overwrite piece sums that a slower workgroup has yet to read
+            if (__builtin_amdgcn_readfirstlane(s_cnt[2 * kGemvWaves])) break;
         }
-        const uint32_t left = end - i;
-        c1 = left < static_cast<uint32_t>(grp.prob[p].nblk) ? static_cast<int>(left) : grp.prob[p].nblk;
-        pc = begin_piece(grp.prob[p], t, 0, c1, lane);
-        if constexpr (kMx) xp = begin_xpiece<B>(grp.prob[p], pc, true);
+    }
+    if constexpr (Chain) {
+        // the last workgroup to finish reports the status and clears the
+        // barrier words for the next launch on the slot (every workgroup has
+        // passed its last wait by then)
+        ChainSync& cs = g_chain_sync[ch.slot];
+        if (threadIdx.x == 0 && dev_add(&cs.exit[0], 1u) + 1u == gridDim.x) {
+            const uint32_t gave_up = dev_load(&cs.expired[0]);
+            if (ch.status)
+                __hip_atomic_store(ch.status, gave_up ? kChainTimeout : 0, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            for (int h = 0; h < 8; ++h) {
+                dev_store(&cs.grp[h][0], 0u);
+                dev_store(&cs.flag[h][0], 0u);
+            }
+            dev_store(&cs.count[0], 0u);
+            // an abandoned launch may leave tiles half counted
+            if (gave_up)
+                for (uint32_t h = 0; h < gridDim.x; ++h) dev_store(counters + h, 0u);
+            dev_store(&cs.expired[0], 0u);
+            dev_store(&cs.exit[0], 0u);
+        }
     }
 }
 

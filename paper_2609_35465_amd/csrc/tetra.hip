@@ -8,6 +8,7 @@
 #include <cmath>
 
 #include <algorithm>
+#include <atomic>
 #include <cstring>
 #include <mutex>
 #include <thread>
@@ -67,7 +68,7 @@ int num_cus(int dev) {
 template <int B>
 int gemv_resident() {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(&tetra_dev::gemv_kernel<B>),
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(&tetra_dev::gemv_kernel<B, true>),
                                                      tetra_dev::kGemvThreads, 0) != hipSuccess)
         return 0;
     return std::max(1, std::min(n, tetra_dev::kGemvGroupsPerCU));
@@ -156,53 +157,87 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) &
 
 int launch_status() { return hipGetLastError() == hipSuccess ? TETRA_OK : TETRA_EDEVICE; }
 
-int launch_gemv(const tetra_gemv_problem* probs, int n, int batch, hipStream_t stream) {
+// polls before a chain barrier wait gives up (about one microsecond each)
+std::atomic<uint32_t> g_chain_wait_limit{1u << 20};
+
+// A plain or grouped product (one phase) or a chain of phases.  Problems are
+// in phase order; phase k holds counts[k] of them.
+int launch_gemv(const tetra_gemv_problem* probs, int n, const int* counts, int n_phases, int batch, int* status,
+                hipStream_t stream) {
     if (!probs || n < 1 || n > TETRA_MAX_GROUP) return TETRA_EINVAL;
+    if (n_phases < 1 || n_phases > TETRA_MAX_PHASES || (n_phases > 1 && !counts)) return TETRA_EINVAL;
     if (batch < 1 || batch > TETRA_MAX_BATCH) return TETRA_EINVAL;
-    tetra_dev::GemvGroup grp;
-    std::memset(&grp, 0, sizeof(grp));
-    unsigned long long total = 0;
-    for (int i = 0; i < n; ++i) {
-        if (total >= (1ull << 31)) return TETRA_EINVAL;
-        const tetra_gemv_problem& q = probs[i];
-        Shape s;
-        if (!q.codes || !q.row_scales || !q.x || !q.y || !shape_of(q.M, q.K, &s)) return TETRA_EINVAL;
-        if (!aligned(q.codes, 16) || !aligned(q.x, 4)) return TETRA_EALIGN;
-        tetra_dev::GemvProblem& P = grp.prob[i];
-        P.codes = static_cast<const uint8_t*>(q.codes);
-        P.sigma = q.row_scales;
-        P.x = q.x;
-        P.y = q.y;
-        P.M = q.M;
-        P.K = q.K;
-        P.nblk = s.nblk;
-        P.T = s.T;
-        P.tail_off = s.tail_off;
-        P.tiles = s.tiles;
-        P.ng = s.nblk / tetra::kGroupCols;
-        P.rem = s.nblk % tetra::kGroupCols;
-        P.blk_base = static_cast<uint32_t>(total);
-        total += static_cast<unsigned long long>(s.tiles) * s.nblk;
+    tetra_dev::GemvChain ch;
+    std::memset(&ch, 0, sizeof(ch));
+    int p = 0;
+    for (int k = 0; k < n_phases; ++k) {
+        const int cnt = counts ? counts[k] : n;
+        if (cnt < 1 || cnt > n - p) return TETRA_EINVAL;
+        unsigned long long total = 0;
+        for (int i = p; i < p + cnt; ++i) {
+            if (total >= (1ull << 31)) return TETRA_EINVAL;
+            const tetra_gemv_problem& q = probs[i];
+            Shape s;
+            if (!q.codes || !q.row_scales || !q.x || !q.y || !shape_of(q.M, q.K, &s)) return TETRA_EINVAL;
+            if (!aligned(q.codes, 16) || !aligned(q.x, 4)) return TETRA_EALIGN;
+            tetra_dev::GemvProblem& P = ch.prob[i];
+            P.codes = static_cast<const uint8_t*>(q.codes);
+            P.sigma = q.row_scales;
+            P.x = q.x;
+            P.y = q.y;
+            P.M = q.M;
+            P.K = q.K;
+            P.nblk = s.nblk;
+            P.T = s.T;
+            P.tail_off = s.tail_off;
+            P.tiles = s.tiles;
+            P.ng = s.nblk / tetra::kGroupCols;
+            P.rem = s.nblk % tetra::kGroupCols;
+            P.blk_base = static_cast<uint32_t>(total);
+            total += static_cast<unsigned long long>(s.tiles) * s.nblk;
+        }
+        if (total >= (1ull << 31)) return TETRA_EINVAL;     // block indices are 32-bit
+        ch.ph[k].p0 = p;
+        ch.ph[k].n = cnt;
+        ch.ph[k].total = static_cast<uint32_t>(total);
+        p += cnt;
     }
-    if (total >= (1ull << 31)) return TETRA_EINVAL;     // block indices are 32-bit
+    if (p != n) return TETRA_EINVAL;
     DeviceState ds;
     int slot = 0;
     if (int st = gemv_slot(stream, &ds, &slot)) return st;
-    grp.n = n;
-    grp.total = static_cast<uint32_t>(total);
     // the workspace slot holds kGemvMaxCUs CUs' worth of workgroups: a larger
     // part runs fewer waves
     const int cus = std::min(ds.cus, tetra_dev::kGemvMaxCUs);
-    grp.waves = std::min(tetra_dev::gemv_waves(grp.total, cus, ds.gemv_groups[batch]),
-                         tetra_dev::gemv_max_groups(batch) * tetra_dev::kGemvWaves);
-    grp.inv_total = 1.0 / static_cast<double>(grp.total);
-    grp.inv_waves = 1.0 / static_cast<double>(grp.waves);
-    grp.slot = slot;
-    const int grid = (grp.waves + tetra_dev::kGemvWaves - 1) / tetra_dev::kGemvWaves;
-#define TETRA_LAUNCH(B)                                                                           \
-    case B:                                                                                       \
-        hipLaunchKernelGGL(tetra_dev::gemv_kernel<B>, dim3(grid), dim3(tetra_dev::kGemvThreads), \
-                           0, stream, grp);                                                       \
+    const int max_waves = std::min(cus * ds.gemv_groups[batch], tetra_dev::gemv_max_groups(batch)) *
+                          tetra_dev::kGemvWaves;
+    int grid;
+    if (n_phases == 1) {
+        ch.ph[0].waves = std::min(tetra_dev::gemv_waves(ch.ph[0].total, cus, ds.gemv_groups[batch]), max_waves);
+        grid = (ch.ph[0].waves + tetra_dev::kGemvWaves - 1) / tetra_dev::kGemvWaves;
+    } else {
+        // every workgroup the device holds at once, so that all of them are
+        // resident together and the barriers between phases can be met
+        grid = max_waves / tetra_dev::kGemvWaves;
+        for (int k = 0; k < n_phases; ++k)
+            ch.ph[k].waves = tetra_dev::chain_phase_waves(ch.ph[k].total, grid * tetra_dev::kGemvWaves);
+    }
+    for (int k = 0; k < n_phases; ++k) {
+        ch.ph[k].inv_total = 1.0 / static_cast<double>(ch.ph[k].total);
+        ch.ph[k].inv_waves = 1.0 / static_cast<double>(ch.ph[k].waves);
+    }
+    ch.n_phases = n_phases;
+    ch.slot = slot;
+    ch.wait_limit = g_chain_wait_limit.load();
+    ch.status = status;
+#define TETRA_LAUNCH(B)                                                                                  \
+    case B:                                                                                              \
+        if (n_phases == 1)                                                                               \
+            hipLaunchKernelGGL((tetra_dev::gemv_kernel<B, false>), dim3(grid), dim3(tetra_dev::kGemvThreads), \
+                               0, stream, ch);                                                           \
+        else                                                                                             \
+            hipLaunchKernelGGL((tetra_dev::gemv_kernel<B, true>), dim3(grid), dim3(tetra_dev::kGemvThreads), \
+                               0, stream, ch);                                                           \
         break;
     switch (batch) {
         TETRA_LAUNCH(1) TETRA_LAUNCH(2) TETRA_LAUNCH(3) TETRA_LAUNCH(4)
@@ -272,6 +307,7 @@ const char* tetra_status_string(int status) {
         case TETRA_EDEVICE: return "HIP runtime error";
         case TETRA_EUNSUPPORTED: return "unsupported request";
         case TETRA_EBUSY: return "every GEMV workspace slot of the device is held by another stream";
+        case TETRA_ETIMEOUT: return "a wait between the phases of a chained product gave up";
         default: return "unknown status";
     }
 }
@@ -364,11 +400,21 @@ int tetra_gemv(const void* codes, const uint16_t* row_scales, const uint16_t* x,
     p.y = y;
     p.M = M;
     p.K = K;
-    return launch_gemv(&p, 1, batch, stream);
+    return launch_gemv(&p, 1, nullptr, 1, batch, nullptr, stream);
 }
 
 int tetra_gemv_grouped(const tetra_gemv_problem* problems, int n, int batch, hipStream_t stream) {
-    return launch_gemv(problems, n, batch, stream);
+    return launch_gemv(problems, n, nullptr, 1, batch, nullptr, stream);
+}
+
+int tetra_gemv_chain(const tetra_gemv_problem* problems, int n, const int* phase_counts, int n_phases, int batch,
+                     int* status, hipStream_t stream) {
+    if (status && !aligned(status, 4)) return TETRA_EALIGN;
+    return launch_gemv(problems, n, phase_counts, n_phases, batch, status, stream);
+}
+
+uint32_t tetra_set_chain_wait_limit(uint32_t polls) {
+    return g_chain_wait_limit.exchange(polls == 0 ? (1u << 20) : polls);
 }
 
 int tetra_decode(const void* words, size_t n, int8_t* y_out, float* blk_scale_out,
@@ -514,6 +560,7 @@ __global__ __launch_bounds__(256) void zero_words_kernel(uint32_t* p, int n) {
 
 int tetra_gemm_noalloc(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K,
                        int N, hipStream_t stream) {
+    static_assert(tetra_dev::kChainTimeout == TETRA_ETIMEOUT, "status value written by the kernel");
     static_assert(kScratchBytes >= (sizeof(uint32_t) * kScratchWorkers + 255) / 256 * 256 +
                                        sizeof(float) * static_cast<size_t>(kScratchWorkers) * 2 * tetra_dev::kPfSlot,
                   "scratch holds the counters and pieces of kScratchWorkers workgroups");

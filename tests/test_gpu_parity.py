@@ -341,6 +341,143 @@ def test_gemv_grouped_sixteen_problems():
         assert float((np.abs(y.cpu().numpy() - yr) / norm).max()) <= TOL_PAPER
 
 
+# ------------------------------------------------ chained phases (one launch)
+
+def _chain_case(shapes_by_phase, batch, seed):
+    """Problems of a chain (phase order), NaN-filled outputs, and the oracle's
+    inputs for each problem."""
+    items, refs, counts = [], [], []
+    for k, shapes in enumerate(shapes_by_phase):
+        counts.append(len(shapes))
+        for j, (M, K) in enumerate(shapes):
+            words, sigma, tail = workloads.tetra_matrix(seed + 31 * k + j, M, K)
+            pk = Packed(words, sigma, tail, K)
+            x = workloads.activations(seed + 1000 + 31 * k + j, batch, K)
+            y = torch.full((batch, M), float("nan"), dtype=torch.float32, device="cuda")
+            items.append((pk.blob, pk.sigma, _f16_dev(x), y, M, K))
+            refs.append((pk, x))
+    return items, refs, counts
+
+
+def _check_chain_outputs(items, refs, rows_of=None, label=""):
+    worst = 0.0
+    for (_, _, _, y, M, K), (pk, x) in zip(items, refs):
+        rows = None if rows_of is None else rows_of(M)
+        yr, norm = ogemv.gemv_f64(pk.words, pk.sigma_h, pk.tail, x, rows=rows)
+        yg = y.cpu().numpy().astype(np.float64)
+        if rows is not None:
+            yg = yg[:, rows]
+        assert not np.isnan(yg).any(), (label, M, K)
+        worst = max(worst, float((np.abs(yg - yr) / np.maximum(norm, 1e-300)).max()))
+    print(f"[chain {label}] worst={worst:.3e}", flush=True)
+    assert worst <= TOL
+    assert worst <= TOL_PAPER
+
+
+_CHAIN_SMALL = [[(300, 24 * 40 + 8), (64, 24 * 40 + 8), (65, 24 * 40 + 8)], [(300, 24 * 12 + 2)],
+                [(1000, 24 * 40 + 8), (999, 24 * 40 + 8)], [(300, 24 * 83 + 16)]]
+
+
+@pytest.mark.parametrize("batch", [1, 2, 3, 4, 8])
+def test_chain_small_every_row(batch):
+    """A decode-step-like chain of four phases (ragged M, tails) in one
+    launch: every row of every product against the oracle; the status word
+    reads 0; a second launch gives the same bits (deterministic split)."""
+    items, refs, counts = _chain_case(_CHAIN_SMALL, batch, 7100 + batch)
+    status = torch.full((1,), 12345, dtype=torch.int32, device="cuda")
+    probs = tt.make_problems(items)
+    print(f"[chain small] batch={batch} phases={counts}", flush=True)
+    tt.gemv_chain(probs, counts, batch, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    _check_chain_outputs(items, refs, label=f"small b{batch}")
+    first = [it[3].clone() for it in items]
+    for it in items:
+        it[3].fill_(float("nan"))
+    tt.gemv_chain(probs, counts, batch, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for a, it in zip(first, items):
+        assert torch.equal(a, it[3])
+
+
+@pytest.mark.parametrize("batch", [1, 4])
+def test_chain_14b_layer_every_row(batch):
+    """One Qwen3-14B-shaped layer as the bench chains it ([q, k, v], [o],
+    [gate, up], [down]): every row of every product against the oracle."""
+    shapes = {n: (M, K) for n, M, K in workloads.layer_shapes("14B")}
+    by_phase = [[shapes["q"], shapes["k"], shapes["v"]], [shapes["o"]], [shapes["gate"], shapes["up"]],
+                [shapes["down"]]]
+    items, refs, counts = _chain_case(by_phase, batch, 7300 + batch)
+    status = torch.full((1,), 12345, dtype=torch.int32, device="cuda")
+    print(f"[chain 14b] batch={batch}", flush=True)
+    tt.gemv_chain(tt.make_problems(items), counts, batch, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    _check_chain_outputs(items, refs, label=f"14b b{batch}")
+
+
+def test_chain_in_graph_replays_match_eager():
+    """A chain captured in a HIP graph: three replays, each after eager work
+    on the same stream, give the eager launch's bits."""
+    items, refs, counts = _chain_case(_CHAIN_SMALL, 1, 7500)
+    probs = tt.make_problems(items)
+    tt.gemv_chain(probs, counts, 1)
+    torch.cuda.synchronize()
+    eager = [it[3].clone() for it in items]
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            tt.gemv_chain(probs, counts, 1, None, s.cuda_stream)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for it in items:
+            it[3].fill_(float("nan"))
+        _ = (torch.ones(1024, device="cuda") * 2).sum()     # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, it in zip(eager, items):
+            assert torch.equal(a, it[3]), rep
+    tt.release_stream(s.cuda_stream)
+
+
+def test_chain_wait_that_gives_up_reports_and_leaves_slot_clean():
+    """A wait limit of one poll, forced from the host, makes the waits between
+    phases give up: the launch still ends, its status word reads
+    TETRA_ETIMEOUT, and the next chain on the same stream (default limit)
+    computes every product correctly with status 0."""
+    items, refs, counts = _chain_case(_CHAIN_SMALL, 1, 7700)
+    probs = tt.make_problems(items)
+    status = torch.full((1,), 12345, dtype=torch.int32, device="cuda")
+    prev = tt.set_chain_wait_limit(1)
+    try:
+        print("[chain timeout] wait limit 1", flush=True)
+        tt.gemv_chain(probs, counts, 1, status)
+        torch.cuda.synchronize()
+    finally:
+        tt.set_chain_wait_limit(prev)
+    assert int(status.item()) == tt.ETIMEOUT
+    for it in items:
+        it[3].fill_(float("nan"))
+    print("[chain timeout] default limit", flush=True)
+    tt.gemv_chain(probs, counts, 1, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    _check_chain_outputs(items, refs, label="after timeout")
+
+
+def test_chain_argument_errors():
+    items, refs, counts = _chain_case([[(64, 48)], [(64, 48)]], 1, 7900)
+    probs = tt.make_problems(items)
+    for bad in ([1], [2, 0], [1, 2], [3]):
+        with pytest.raises(tt.TetraError):
+            tt.gemv_chain(probs, bad, 1)
+
+
 def _sample_rows(M, rng, n=192):
     rows = set(range(min(M, 64))) | {M - 1, M - 2, M // 2}
     rows |= set(rng.choice(M, size=min(n, M), replace=False).tolist())
