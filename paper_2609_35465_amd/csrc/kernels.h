@@ -294,8 +294,10 @@ struct GemvProblem {
 struct GemvSplit {
     double inv_total, inv_waves;   // 1 / total, 1 / waves
     uint32_t total;                // blocks in the phase (< 2^31)
-    int waves;                     // waves that take a range (the launch's first `waves`)
+    int waves;                     // waves that take a range
+    int wpg;                       // of them per workgroup: wave v is wave v mod wpg of workgroup v / wpg
     int p0, n;                     // its problems: prob[p0 .. p0 + n - 1]
+    int aligned;                   // 1: tile-aligned split (below), 0: even split of the block sequence
 };
 
 constexpr int kMaxPhases = 16;
@@ -398,13 +400,15 @@ inline int gemv_waves(uint32_t total, int cus, int groups) {
     return static_cast<int>(want < cap ? want : cap);
 }
 
-// Waves of one phase of a chain: its launch holds a whole round of
-// workgroups anyway, and the tables are staged once for all phases, so a
-// wave is worth fewer blocks than in a single launch.
-constexpr uint32_t kChainMinBlocks = 4;
-inline int chain_phase_waves(uint32_t total, int launch_waves) {
-    const uint32_t want = total / kChainMinBlocks > 0 ? total / kChainMinBlocks : 1u;
-    return static_cast<int>(want < static_cast<uint32_t>(launch_waves) ? want : static_cast<uint32_t>(launch_waves));
+// Waves per workgroup in one phase of a chain: its launch holds a whole
+// round of workgroups anyway, and the tables are staged once for all phases,
+// so a wave is worth fewer blocks than in a single launch (at least
+// kChainMinBlocks each, up to all kGemvWaves).
+constexpr uint32_t kChainMinBlocks = 8;
+inline int chain_phase_wpg(uint32_t total, int groups) {
+    const unsigned long long per = static_cast<unsigned long long>(kChainMinBlocks) * static_cast<uint32_t>(groups);
+    const unsigned long long w = (total + per - 1) / per;
+    return static_cast<int>(w < 1 ? 1 : w > static_cast<unsigned long long>(kGemvWaves) ? kGemvWaves : w);
 }
 
 // largest workgroup count of a launch at batch B that the slot's partial
@@ -433,6 +437,19 @@ __device__ __forceinline__ int wave_of(uint32_t i, const GemvSplit& sp) {
     return static_cast<int>(div_exact(static_cast<unsigned long long>(i + 1) * static_cast<uint32_t>(sp.waves) - 1,
                                       sp.total, sp.inv_total));
 }
+
+// Tile-aligned split (when every tile can have a wave of its own): the
+// waves are shared out over the tiles in proportion to their blocks, tile u
+// (first block B_u) taking waves floor(B_u W / total) .. floor((B_u + nblk) W
+// / total) - 1, and each tile's columns are split evenly over its waves.
+// Every wave then holds one piece of one tile, so no wave waits for the
+// reduction of one tile before it starts the next.  The first wave of the
+// tile that starts at block t0:
+__device__ __forceinline__ int tile_first_wave(uint32_t t0, const GemvSplit& sp) {
+    return static_cast<int>(div_exact(static_cast<unsigned long long>(t0) * static_cast<uint32_t>(sp.waves),
+                                      sp.total, sp.inv_total));
+}
+
 
 // code words of one item (a group of four block columns, or the nblk mod 4
 // single columns of a tile): the 16-bit part of block k is in hi.x (k = 0,
@@ -1064,13 +1081,29 @@ struct RangePos {
     bool live;
 };
 
-__device__ __forceinline__ RangePos range_pos(const GemvChain& ch, int k, int w) {
+__device__ __forceinline__ RangePos range_pos(const GemvChain& ch, int k, int g, int wid) {
     const GemvSplit& sp = ch.ph[k];
+    const int w = g * sp.wpg + wid;
     RangePos r;
-    r.live = w < sp.waves;
+    r.live = wid < sp.wpg && w < sp.waves;
     const int wr = r.live ? w : sp.waves - 1;
-    r.i = __builtin_amdgcn_readfirstlane(range_begin(wr, sp));
-    r.end = __builtin_amdgcn_readfirstlane(range_begin(wr + 1, sp));
+    if (sp.aligned) {
+        // the tile of wave wr holds block floor(((wr + 1) total - 1) / W)
+        const uint32_t bs = div_exact(static_cast<unsigned long long>(wr + 1) * sp.total - 1,
+                                      static_cast<uint32_t>(sp.waves), sp.inv_waves);
+        int q = sp.p0;
+        while (q + 1 < sp.p0 + sp.n && bs >= ch.prob[q + 1].blk_base) ++q;
+        const uint32_t nb = static_cast<uint32_t>(ch.prob[q].nblk);
+        const uint32_t t0 = ch.prob[q].blk_base + (bs - ch.prob[q].blk_base) / nb * nb;
+        const int wa = tile_first_wave(t0, sp);
+        const uint32_t n = static_cast<uint32_t>(tile_first_wave(t0 + nb, sp) - wa);
+        const uint32_t j = static_cast<uint32_t>(wr - wa);
+        r.i = __builtin_amdgcn_readfirstlane(t0 + j * nb / n);
+        r.end = __builtin_amdgcn_readfirstlane(t0 + (j + 1) * nb / n);
+    } else {
+        r.i = __builtin_amdgcn_readfirstlane(range_begin(wr, sp));
+        r.end = __builtin_amdgcn_readfirstlane(range_begin(wr + 1, sp));
+    }
     int p = sp.p0;
     while (p + 1 < sp.p0 + sp.n && r.i >= ch.prob[p + 1].blk_base) ++p;
     r.p = p;
@@ -1088,7 +1121,8 @@ __device__ __forceinline__ RangePos range_pos(const GemvChain& ch, int k, int w)
 // in wave order), and when the tile reaches into other workgroups each
 // workgroup's sum goes to the workspace, where the last workgroup to arrive
 // adds them in workgroup order.  Piece p of a wave's range: its sum, then
-// its share of the tile's reduction.
+// its share of the tile's reduction.  w0: the workgroup's first wave of the
+// phase (g * wpg).
 template <int B>
 __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSplit& sp, int t, int c, int c1,
                                              bool first, const float (&sum)[B], int w0, int g, float* s_piece,
@@ -1099,13 +1133,21 @@ __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSpl
         return;
     }
     const int wid = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
-    const int wlast = min(w0 + kGemvWaves, sp.waves) - 1;
+    const int wlast = min(w0 + sp.wpg, sp.waves) - 1;
     const uint32_t t0 = P.blk_base + static_cast<uint32_t>(t) * P.nblk;
-    const int wa = __builtin_amdgcn_readfirstlane(wave_of(t0, sp));
-    const int wb = __builtin_amdgcn_readfirstlane(wave_of(t0 + P.nblk - 1, sp));
-    // slot of wave v's piece of this tile: 0 when the tile is where v's range
-    // starts, which holds for every contributor but possibly the first
-    const int slot_wa = __builtin_amdgcn_readfirstlane(range_begin(wa, sp) >= t0 ? 0 : 1);
+    // the tile's contributors wa..wb; slot of wave v's piece of this tile: 0
+    // when the tile is where v's range starts, which holds for every
+    // contributor but possibly the first (always, in a tile-aligned split)
+    int wa, wb, slot_wa;
+    if (sp.aligned) {
+        wa = __builtin_amdgcn_readfirstlane(tile_first_wave(t0, sp));
+        wb = __builtin_amdgcn_readfirstlane(tile_first_wave(t0 + P.nblk, sp)) - 1;
+        slot_wa = 0;
+    } else {
+        wa = __builtin_amdgcn_readfirstlane(wave_of(t0, sp));
+        wb = __builtin_amdgcn_readfirstlane(wave_of(t0 + P.nblk - 1, sp));
+        slot_wa = __builtin_amdgcn_readfirstlane(range_begin(wa, sp) >= t0 ? 0 : 1);
+    }
     auto slot_of = [&](int v) { return v > wa ? 0 : slot_wa; };
     const int a = max(wa, w0), b = min(wb, wlast);
     const int ln = lane_now();
@@ -1138,8 +1180,11 @@ __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSpl
     // Workgroup sums and counters are accessed only with device-scope
     // atomics, which are coherent across the chip's L2 caches; the wait
     // orders the sum before the count.
-    const int ga = wa / kGemvWaves, gb = wb / kGemvWaves;
-    const int gslot_ga = __builtin_amdgcn_readfirstlane(range_begin(ga * kGemvWaves, sp) >= t0 ? 0 : 1);
+    const int ga = wa / sp.wpg, gb = wb / sp.wpg;
+    // slot 0 holds the tile reaching in from earlier workgroups, slot 1 one
+    // that starts inside the workgroup and reaches past it
+    const int gslot_ga = sp.aligned ? (ga * sp.wpg >= wa ? 0 : 1)
+                                    : __builtin_amdgcn_readfirstlane(range_begin(ga * sp.wpg, sp) >= t0 ? 0 : 1);
     auto gslot_of = [&](int h) { return h > ga ? 0 : gslot_ga; };
     float* gp = partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + ln;
 #pragma unroll
@@ -1150,8 +1195,9 @@ __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSpl
     if (ln == 0) garr = __hip_atomic_fetch_add(counters + gb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     garr = __builtin_amdgcn_readfirstlane(garr);
     if (garr != static_cast<uint32_t>(gb - ga)) return;
+    float out[B];
 #pragma unroll
-    for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
+    for (int bb = 0; bb < B; ++bb) out[bb] = 0.f;
     // loads in batches of eight, added in workgroup order
     for (int h0 = ga; h0 <= gb; h0 += 8) {
         float pv[8][B];
@@ -1169,11 +1215,11 @@ __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSpl
         for (int u = 0; u < 8; ++u)
             if (h0 + u <= gb) {
 #pragma unroll
-                for (int bb = 0; bb < B; ++bb) tot[bb] += pv[u][bb];
+                for (int bb = 0; bb < B; ++bb) out[bb] += pv[u][bb];
             }
     }
     if (ln == 0) __hip_atomic_store(counters + gb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    store_rows<B>(P, t, tot, rt);
+    store_rows<B>(P, t, out, rt);
 }
 
 // The whole launch: decoder tables staged once, then the phases in order (one
@@ -1195,15 +1241,13 @@ void gemv_kernel(const GemvChain ch) {
     const int lane = threadIdx.x & 63;
     const int wid = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
     const int g = static_cast<int>(blockIdx.x);
-    const int w0 = g * kGemvWaves;
-    const int w = w0 + wid;
     TableStage<kGemvThreads> ts;
     ts.load();
     uint32_t* const counters = g_gemv_slots[ch.slot].counters;
     float* const partials = g_gemv_slots[ch.slot].partials;
     // the first piece's code words are requested while the tables arrive;
     // the barrier orders LDS only, so they stay in flight across it
-    RangePos r = range_pos(ch, 0, w);
+    RangePos r = range_pos(ch, 0, g, wid);
     int p = r.p, t = r.t, c = r.c, c1 = r.c1;
     uint32_t i = r.i, end = r.end;
     Piece pc = begin_piece_live(ch.prob[p], t, c, c1, lane, r.live);
@@ -1226,7 +1270,8 @@ void gemv_kernel(const GemvChain ch) {
             float sum[B];
             if constexpr (kMx) run_piece_mx<B>(P, pc, xp, L, xs, sum);
             else run_piece<B>(P, pc, L, sum);
-            finish_piece<B>(P, ch.ph[k], t, c, c1, first, sum, w0, g, s_piece, s_cnt, counters, partials);
+            finish_piece<B>(P, ch.ph[k], t, c, c1, first, sum, g * ch.ph[k].wpg, g, s_piece, s_cnt, counters,
+                            partials);
             i += static_cast<uint32_t>(c1 - c);
             if (i < end) {
                 first = false;
@@ -1247,7 +1292,7 @@ void gemv_kernel(const GemvChain ch) {
         } else {
             // the wave's range of phase k is done
             if (++k == ch.n_phases) break;
-            r = range_pos(ch, k, w);
+            r = range_pos(ch, k, g, wid);
             p = r.p;
             t = r.t;
             c = r.c;

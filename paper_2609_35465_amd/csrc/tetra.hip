@@ -214,17 +214,31 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, const int* counts, int n
     int grid;
     if (n_phases == 1) {
         ch.ph[0].waves = std::min(tetra_dev::gemv_waves(ch.ph[0].total, cus, ds.gemv_groups[batch]), max_waves);
+        ch.ph[0].wpg = tetra_dev::kGemvWaves;
         grid = (ch.ph[0].waves + tetra_dev::kGemvWaves - 1) / tetra_dev::kGemvWaves;
     } else {
         // every workgroup the device holds at once, so that all of them are
-        // resident together and the barriers between phases can be met
+        // resident together and the barriers between phases can be met; a
+        // phase takes the same number of waves from every workgroup, so that
+        // every CU gets the same share of it
         grid = max_waves / tetra_dev::kGemvWaves;
-        for (int k = 0; k < n_phases; ++k)
-            ch.ph[k].waves = tetra_dev::chain_phase_waves(ch.ph[k].total, grid * tetra_dev::kGemvWaves);
+        for (int k = 0; k < n_phases; ++k) {
+            ch.ph[k].wpg = tetra_dev::chain_phase_wpg(ch.ph[k].total, grid);
+            ch.ph[k].waves = static_cast<int>(std::min<uint32_t>(ch.ph[k].total,
+                                                                 static_cast<uint32_t>(grid * ch.ph[k].wpg)));
+        }
     }
     for (int k = 0; k < n_phases; ++k) {
-        ch.ph[k].inv_total = 1.0 / static_cast<double>(ch.ph[k].total);
-        ch.ph[k].inv_waves = 1.0 / static_cast<double>(ch.ph[k].waves);
+        tetra_dev::GemvSplit& sp = ch.ph[k];
+        sp.inv_total = 1.0 / static_cast<double>(sp.total);
+        sp.inv_waves = 1.0 / static_cast<double>(sp.waves);
+        // tile-aligned when every tile gets a wave of its own (W nblk >= total
+        // for the smallest nblk of the phase); waves <= total keeps every
+        // tile's share at most its columns, so no range is empty
+        int nblk_min = INT_MAX;
+        for (int i = sp.p0; i < sp.p0 + sp.n; ++i) nblk_min = std::min(nblk_min, ch.prob[i].nblk);
+        sp.aligned = static_cast<unsigned long long>(sp.waves) * static_cast<unsigned>(nblk_min) >= sp.total &&
+                     static_cast<uint32_t>(sp.waves) <= sp.total;
     }
     ch.n_phases = n_phases;
     ch.slot = slot;
