@@ -48,19 +48,28 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--chain-layers", type=int, default=1,
-                    help="--mode chain: layers per launch (1 or 2)")
-    ap.add_argument("--mode", default="deps", choices=["matrix", "deps", "layer", "chain"],
+    ap.add_argument("--chain-layers", type=int, default=2,
+                    help="--mode chain: layers per launch (1 or 2: a launch holds at most 16 matrices)")
+    ap.add_argument("--no-deps-figure", action="store_true",
+                    help="--mode chain: skip timing the same step as 160 separate launches")
+    ap.add_argument("--mode", default="chain", choices=["matrix", "deps", "layer", "chain"],
                     help="matrix: one launch per matrix; deps: per layer [q,k,v] [o] "
-                         "[gate,up] [down] (the launches a decode step can fuse); "
-                         "layer: one grouped launch per layer")
-    ap.add_argument("--workload", default="tetra", choices=["tetra", "c4", "head", "rotate", "prefill", "encode"],
+                         "[gate,up] [down] as four launches (the dependency groups of a "
+                         "decode step); chain: the same groups as the phases of one "
+                         "tetra_gemv_chain launch per --chain-layers layers, each phase "
+                         "starting after the one before has finished on every workgroup; "
+                         "layer: one grouped launch per layer (not a legal decode order)")
+    ap.add_argument("--workload", default="tetra",
+                    choices=["tetra", "c4", "head", "rotate", "prefill", "encode", "single", "stream"],
                     help="tetra: every projection a Tetra matrix (the GEMV metric); c4: the "
                          "full decode step -- 10%% of the projections (seeded) stored as int4 "
                          "w4g128 and one 4-bit embedding row gathered per step; head: the "
                          "4-bit output head GEMV (151936 x 5120, groups of 64) alone; rotate: "
                          "the online activation rotations of one layer; prefill: a 203-token "
-                         "prompt through the Tetra projections on the matrix cores")
+                         "prompt through the Tetra projections on the matrix cores; single: "
+                         "the one 1536 x 1536 matrix at batch 1, over distinct copies (cold "
+                         "buffers); stream: the achievable HBM read rate of this GPU (a "
+                         "plain reduction over distinct buffers, no Tetra code)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the benchmark: copy a buffer of this many MiB five "
                          "times with torch (a plain copy kernel of known size, the "
@@ -262,41 +271,115 @@ def parity_spot_check_int4(torch, plan):
     return worst
 
 
-def cpu_baseline(torch, tt, plan, seconds):
-    """The CPU oracle (float64 numpy, one thread) over the step's matrices in
-    step order, 2048 rows at a time, until it has run for `seconds`; rate in
-    GB/s of Tetra bytes (6 B per block, 2 B per tail weight and row scale).
-    Copying a matrix to the host and unpacking it are not timed."""
+_CPU_DATA = []
+
+
+def _cpu_init(paths):
+    """Pool worker set-up: memory-map the host copies of the sampled matrices."""
+    global _CPU_DATA
+    _CPU_DATA = [tuple(np.load(os.path.join(d, f + ".npy"), mmap_mode="r") for f in ("w", "s", "t", "x"))
+                 for d in paths]
+
+
+def _cpu_task(task):
+    """One chunk of rows of one sampled matrix through the oracle."""
     from oracle import gemv as ogemv
-    t_used, bytes_done, rows_done, mats = 0.0, 0, 0, []
-    for m, x, _ in plan:
-        if t_used >= seconds:
-            break
-        if not isinstance(m, Matrix):
-            continue
-        blob = m.blob.cpu().numpy()
-        words, tail = tt.unpack_rows(blob, m.M, m.K)
-        sig = m.sigma.cpu().numpy()
-        xh = x.cpu().numpy()
-        done = 0
-        for r0 in range(0, m.M, 2048):
-            if t_used >= seconds:
+    mi, r0, r1 = task
+    words, sig, tail, x = _CPU_DATA[mi]
+    ogemv.gemv_f64(words, sig, tail if tail.size else None, x, rows=np.arange(r0, r1))
+    return mi, r1 - r0
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(torch, tt, plan, seconds):
+    """The CPU oracle as it stands (float64 numpy, oracle.gemv.gemv_f64) over
+    the step's matrices in step order, 2048 rows per task, run by a pool of
+    worker processes on the host's cores (at most 16, the host share of one
+    GPU), until about `seconds` of wall time; rate in GB/s of Tetra bytes
+    (6 B per block, 2 B per tail weight and row scale).  A single-process run
+    on the first matrix first gives the one-core rate and sizes the sample.
+    Copying matrices to the host and unpacking them are not timed."""
+    import multiprocessing as mp
+    import shutil
+    import tempfile
+    from oracle import gemv as ogemv
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    tmp = tempfile.mkdtemp(prefix="tetra_cpu_")
+    try:
+        paths, sizes, names = [], [], []
+
+        def host_copy(m, x):
+            d = os.path.join(tmp, str(len(paths)))
+            os.makedirs(d)
+            words, tail = tt.unpack_rows(m.blob.cpu().numpy(), m.M, m.K)
+            np.save(os.path.join(d, "w.npy"), words)
+            np.save(os.path.join(d, "s.npy"), m.sigma.cpu().numpy())
+            np.save(os.path.join(d, "t.npy"), tail if tail is not None else np.zeros((0,), np.float16))
+            np.save(os.path.join(d, "x.npy"), x.cpu().numpy())
+            paths.append(d)
+            sizes.append(m.nblk * 6 + 2 * m.T + 2)
+            names.append(f"{m.name} {m.M}x{m.K}")
+
+        tetra = [(m, x) for m, x, _ in plan if isinstance(m, Matrix)]
+        host_copy(*tetra[0])
+        # one core: rows of the first matrix for about a tenth of the budget
+        _cpu_init(paths)
+        M0 = tetra[0][0].M
+        t0, rows1 = time.perf_counter(), 0
+        while time.perf_counter() - t0 < seconds / 10:
+            r0 = rows1 % M0
+            _cpu_task((0, r0, min(r0 + 2048, M0)))
+            rows1 += min(r0 + 2048, M0) - r0
+        t1 = time.perf_counter() - t0
+        rate1 = rows1 * sizes[0] / t1
+        # the pool's sample: the step's matrices in order, about `seconds` of
+        # work (at most 24 matrices), cycled through until the time is used
+        want = rate1 * cores * seconds
+        have = tetra[0][0].M * sizes[0]
+        for m, x in tetra[1:24]:
+            if have >= want:
                 break
-            rows = np.arange(r0, min(r0 + 2048, m.M))
+            host_copy(m, x)
+            have += m.M * sizes[-1]
+        chunks = [(i, r0, min(r0 + 2048, tetra[i][0].M)) for i in range(len(paths))
+                  for r0 in range(0, tetra[i][0].M, 2048)]
+        ctx = mp.get_context("spawn")
+        with ctx.Pool(cores, initializer=_cpu_init, initargs=(paths,)) as pool:
+            pool.map(_cpu_task, [(0, 0, 1)] * cores)          # workers up and warm
+            done_rows = [0] * len(paths)
+            pending, k = [], 0
             t0 = time.perf_counter()
-            ogemv.gemv_f64(words, sig, tail, xh, rows=rows)
-            t_used += time.perf_counter() - t0
-            done += len(rows)
-            bytes_done += len(rows) * (m.nblk * 6 + 2 * m.T + 2)
-        rows_done += done
-        mats.append(f"{m.name} {m.M}x{m.K}" + ("" if done == m.M else f" ({done} rows)"))
-    return {
-        "value": round(bytes_done / t_used / 1e9, 6), "unit": "GB/s", "cores": 1,
-        "kind": "oracle",
-        "sample": f"{len(mats)} matrices of the step in step order "
-                  f"[{', '.join(mats)}], {rows_done} rows in {t_used:.1f} s, "
-                  f"float64 numpy, batch {plan[0][1].shape[0]}",
-    }
+            # two chunks in flight per worker, new ones only while time is left
+            while True:
+                while len(pending) < 2 * cores and time.perf_counter() - t0 < seconds:
+                    pending.append(pool.apply_async(_cpu_task, (chunks[k % len(chunks)],)))
+                    k += 1
+                if not pending:
+                    break
+                mi, n = pending.pop(0).get()
+                done_rows[mi] += n
+            wall = time.perf_counter() - t0
+        bytes_done = sum(r * sz for r, sz in zip(done_rows, sizes))
+        return {
+            "value": round(bytes_done / wall / 1e9, 6), "unit": "GB/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"the first {len(paths)} matrices of the step in step order "
+                      f"[{', '.join(names[:7])}{', ...' if len(names) > 7 else ''}], cycled: "
+                      f"{sum(done_rows)} rows in {wall:.1f} s on {cores} worker processes, float64 numpy "
+                      f"(oracle.gemv.gemv_f64), batch {plan[0][1].shape[0]}; host CPU {cpu_model()}",
+            "single_core_gbs": round(rate1 / 1e9, 6),
+        }
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
 
 
 KERNEL_SOURCES = ("paper_2609_35465_amd/csrc/kernels.h", "paper_2609_35465_amd/csrc/device_tables.h",
@@ -691,6 +774,109 @@ def main_encode(args, torch, tt):
     return 0
 
 
+def main_single(args, torch, tt):
+    """The one 1536 x 1536 matrix at batch 1 (the smallest configuration):
+    one tetra_gemv per launch, over enough distinct copies of the packed
+    matrix (at least 1 GiB) that no launch finds its codes in a cache;
+    the launches run back to back in a HIP graph."""
+    from oracle import gemv as ogemv
+    stream = torch.cuda.current_stream()
+    gen = torch.Generator(device="cuda").manual_seed(3)
+    from paper_2609_35465_amd import workloads
+    name, M, K = workloads.single_shape()[0]
+    m = Matrix(torch, tt, name, M, K, gen, workloads.seed_for(0, 0))
+    x = torch.randn(args.batch, K, generator=gen, device="cuda").half()
+    n_copies = -(-(1 << 30) // m.blob.numel())
+    blobs = [m.blob.clone() for _ in range(n_copies)]
+    y = torch.full((args.batch, M), float("nan"), dtype=torch.float32, device="cuda")
+    tt.gemv(blobs[0], m.sigma, x, y, M, K, args.batch)
+    torch.cuda.synchronize()
+    words, tail = tt.unpack_rows(m.blob.cpu().numpy(), M, K)
+    ref, norm = ogemv.gemv_f64(words, m.sigma.cpu().numpy(), tail, x.cpu().numpy())
+    parity = float((np.abs(y.cpu().numpy().astype(np.float64) - ref) / norm).max())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for b in blobs:
+            tt.gemv(b, m.sigma, x, y, M, K, args.batch, torch.cuda.current_stream().cuda_stream)
+    for _ in range(max(1, args.warmup)):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = max(1, args.steps // 4)
+    e0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_launch = e0.elapsed_time(e1) / (reps * n_copies)
+    algo = m.read_bytes + 2 * K * args.batch + 4 * M * args.batch
+    value = algo / (ms_launch * 1e-3) / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": reps * n_copies,
+        "warmup": args.warmup, "ms_per_step": round(ms_launch, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16-in/f32-acc", "data": "synthetic",
+        "config": {"workload": f"single Tetra GEMV {M} x {K}, batch {args.batch}, over {n_copies} distinct "
+                               f"copies of the packed matrix ({n_copies * m.blob.numel() / 2**30:.2f} GiB), "
+                               f"one launch per step", "batch": args.batch, "hip_graph": True},
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "bits_read_per_weight": round(m.read_bytes * 8 / m.weights, 4),
+        "weights_per_s": round(m.weights / (ms_launch * 1e-3), 1),
+        "parity_worst_rel_err": parity,
+        "roofline": {"bound": "hbm", "achieved": round(value, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(value / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "gemv_kernel",
+                     "avg_launch_us": round(ms_launch * 1e3, 3), "bytes_per_launch": algo},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(torch, tt, [(m, x, y)], args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def main_stream(args, torch):
+    """The achievable HBM read rate of this GPU: torch row sums (rows of 4096
+    fp32) over 8 distinct 256 MiB buffers (2 GiB in all, far above the
+    256 MB last-level cache), one kernel per buffer, back to back on one
+    stream; outputs are 1/4096 of the bytes read.  A plain copy of the same
+    buffers (read and write counted) is reported beside it."""
+    stream = torch.cuda.current_stream()
+    n, each, row = 8, 256 << 20, 4096
+    bufs = [torch.empty(each // 4, dtype=torch.float32, device="cuda").uniform_().view(-1, row) for _ in range(n)]
+    outs = [torch.empty(each // 4 // row, dtype=torch.float32, device="cuda") for _ in range(n)]
+    dsts = [torch.empty_like(bufs[0]) for _ in range(2)]
+
+    def reads():
+        for b, o in zip(bufs, outs):
+            torch.sum(b, 1, out=o)
+
+    def copies():
+        for i, b in enumerate(bufs):
+            dsts[i % 2].copy_(b)
+
+    def timed(fn):
+        for _ in range(max(1, args.warmup)):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    ms = timed(reads)
+    value = n * each / (ms * 1e-3) / 1e9
+    ms_copy = timed(copies)
+    print(json.dumps({"metric": "achievable HBM read GB/s (torch row sums over 2 GiB of distinct buffers)",
+                      "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+                      "ms_per_step": round(ms, 4), "higher_is_better": True,
+                      "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2), "data": "synthetic",
+                      "copy_gbs_read_plus_write": round(2 * n * each / (ms_copy * 1e-3) / 1e9, 2),
+                      "config": {"workload": "read-only streaming probe", "buffers": n, "buffer_bytes": each,
+                                 "row_elements": row}}), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -721,6 +907,10 @@ def main():
         return main_prefill(args, torch, tt)
     if args.workload == "encode":
         return main_encode(args, torch, tt)
+    if args.workload == "single":
+        return main_single(args, torch, tt)
+    if args.workload == "stream":
+        return main_stream(args, torch)
     stream = torch.cuda.current_stream()
     plan, L, emb = build_workload(torch, tt, args.model, args.layers, args.batch, args.workload)
     torch.cuda.synchronize()
@@ -790,6 +980,22 @@ def main():
     achieved = (tetra_bytes / n_tetra) / (avg_launch_ms * 1e-3) / 1e9
     traffic = recorded_traffic(args, L)
 
+    # beside a chained step, the same step as separate launches (one per
+    # dependency group: 160 for the 14B set), labelled as such
+    deps_fig = None
+    if args.mode == "chain" and not args.no_deps_figure:
+        dl = build_launches(tt, plan, "deps", emb=emb)
+        if graph is not None:
+            gd = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gd):
+                run_step(tt, dl, args.batch, torch.cuda.current_stream().cuda_stream)
+            ms_deps = timed(gd.replay, args.steps)
+        else:
+            ms_deps = timed(lambda: run_step(tt, dl, args.batch, stream.cuda_stream), args.steps)
+        deps_fig = {"launch_grouping": "deps", "launches_per_step": len(dl),
+                    "ms_per_step": round(ms_deps, 4),
+                    "value": round(algo_bytes / (ms_deps * 1e-3) / 1e9, 2), "unit": "GB/s"}
+
     value = algo_bytes / (ms_step * 1e-3) / 1e9
     bits_w = bytes_read * 8 / weights
     out = {
@@ -824,6 +1030,7 @@ def main():
         "token_equiv_latency_ms": round(ms_step, 4),
         "parity_worst_rel_err": parity,
         "parity_int4_worst_rel_err": parity_int4,
+        "separate_launches": deps_fig,
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
             "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
