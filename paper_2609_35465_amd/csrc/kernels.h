@@ -298,6 +298,7 @@ struct GemvSplit {
     int wpg;                       // of them per workgroup: wave v is wave v mod wpg of workgroup v / wpg
     int p0, n;                     // its problems: prob[p0 .. p0 + n - 1]
     int aligned;                   // 1: tile-aligned split (below), 0: even split of the block sequence
+    int defer;                     // 1: tiles that span workgroups are added up after the next barrier
 };
 
 constexpr int kMaxPhases = 16;
@@ -311,6 +312,7 @@ struct GemvChain {
     GemvProblem prob[kMaxGroup];   // blk_base counts from the start of the problem's phase
     GemvSplit ph[kMaxPhases];
     int n_phases;
+    int buffers;                   // partial-sum buffers the phases rotate over: 1, or kChainBuffers
     int slot;                      // workspace slot of the launch (g_gemv_slots, g_chain_sync)
     uint32_t wait_limit;           // polls before a chain barrier wait gives up
     int* status;                   // device word for the launch's status, or null
@@ -410,6 +412,14 @@ inline int chain_phase_wpg(uint32_t total, int groups) {
     const unsigned long long w = (total + per - 1) / per;
     return static_cast<int>(w < 1 ? 1 : w > static_cast<unsigned long long>(kGemvWaves) ? kGemvWaves : w);
 }
+
+// Partial-sum buffers of a chain whose phases defer (when three fit in the
+// slot; otherwise every phase uses the one buffer and none defers): phase k
+// writes buffer k mod 3.  A deferred phase's sums are read while the phase
+// after it runs, and buffer k mod 3 is written again only by phase k + 3,
+// which starts after every workgroup has arrived at the barrier that follows
+// phase k + 1, and so after every read of phase k's sums.
+constexpr int kChainBuffers = 3;
 
 // largest workgroup count of a launch at batch B that the slot's partial
 // sums hold
@@ -1116,17 +1126,66 @@ __device__ __forceinline__ RangePos range_pos(const GemvChain& ch, int k, int g,
     return r;
 }
 
+// A tile of a deferred phase whose workgroup sums its first workgroup's last
+// wave adds up later: problem p, tile t, workgroups ga..gb, the slot of ga's
+// sum.  Packed into two wave-uniform words; p < 0: none.
+struct Pending {
+    int p, t, ga, gb, gs;
+};
+
+__device__ __forceinline__ Pending no_pending() { return Pending{-1, 0, 0, 0, 0}; }
+
+// the workgroup sums ga..gb of tile t (slot gs for ga, 0 for the others),
+// added in workgroup order, times sigma, plus the tail, into y
+template <int B>
+__device__ __forceinline__ void combine_groups(const GemvProblem& P, int t, int ga, int gb, int gs,
+                                               const float* partials) {
+    const int ln = lane_now();
+    const RowTail rt = load_rows(P, t);   // in flight while the sums combine
+    auto gslot_of = [&](int h) { return h > ga ? 0 : gs; };
+    float out[B];
+#pragma unroll
+    for (int bb = 0; bb < B; ++bb) out[bb] = 0.f;
+    // loads in batches of eight, added in workgroup order
+    for (int h0 = ga; h0 <= gb; h0 += 8) {
+        float pv[8][B];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int h = h0 + u;
+            if (h <= gb) {
+                const float* ph = partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + ln;
+#pragma unroll
+                for (int bb = 0; bb < B; ++bb)
+                    pv[u][bb] = __hip_atomic_load(ph + bb * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (h0 + u <= gb) {
+#pragma unroll
+                for (int bb = 0; bb < B; ++bb) out[bb] += pv[u][bb];
+            }
+    }
+    store_rows<B>(P, t, out, rt);
+}
+
 // Pieces of a tile are combined in two levels: the waves of one workgroup
 // that hold pieces of the tile add them in LDS (the last of them to arrive,
 // in wave order), and when the tile reaches into other workgroups each
 // workgroup's sum goes to the workspace, where the last workgroup to arrive
-// adds them in workgroup order.  Piece p of a wave's range: its sum, then
-// its share of the tile's reduction.  w0: the workgroup's first wave of the
+// adds them in workgroup order.  In a deferred phase no workgroup waits
+// for the others: the workgroup sums are complete at the next chain
+// barrier, and the wave that wrote the first workgroup's sum adds them up
+// while it waits at the barrier after that (or at the launch's end), which
+// takes two device-wide round trips (a counter and the loads) off the
+// phase's end.  Piece p (problem index) of a wave's range: its sum, then its
+// share of the tile's reduction.  w0: the workgroup's first wave of the
 // phase (g * wpg).
 template <int B>
-__device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSplit& sp, int t, int c, int c1,
-                                             bool first, const float (&sum)[B], int w0, int g, float* s_piece,
-                                             uint32_t* s_cnt, uint32_t* counters, float* partials) {
+__device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSplit& sp, int p, int t, int c,
+                                             int c1, bool first, const float (&sum)[B], int w0, int g,
+                                             float* s_piece, uint32_t* s_cnt, uint32_t* counters, float* partials,
+                                             Pending& pend) {
     if (c == 0 && c1 == P.nblk) {
         const RowTail rt = load_rows(P, t);
         store_rows<B>(P, t, sum, rt);
@@ -1163,7 +1222,9 @@ __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSpl
     arrived = __builtin_amdgcn_readfirstlane(arrived);
     if (arrived != static_cast<uint32_t>(b - a)) return;
     // last of this workgroup's pieces of the tile: add them in wave order
-    const RowTail rt = load_rows(P, t);   // in flight while the sums combine
+    const bool inside = wa >= w0 && wb <= wlast;   // the tile lies in this workgroup
+    RowTail rt;
+    if (inside) rt = load_rows(P, t);   // in flight while the sums combine
     float tot[B];
 #pragma unroll
     for (int bb = 0; bb < B; ++bb) tot[bb] = 0.f;
@@ -1172,7 +1233,7 @@ __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSpl
 #pragma unroll
         for (int bb = 0; bb < B; ++bb) tot[bb] += pv[bb * 64];
     }
-    if (wa >= w0 && wb <= wlast) {
+    if (inside) {
         store_rows<B>(P, t, tot, rt);
         return;
     }
@@ -1185,41 +1246,21 @@ __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSpl
     // that starts inside the workgroup and reaches past it
     const int gslot_ga = sp.aligned ? (ga * sp.wpg >= wa ? 0 : 1)
                                     : __builtin_amdgcn_readfirstlane(range_begin(ga * sp.wpg, sp) >= t0 ? 0 : 1);
-    auto gslot_of = [&](int h) { return h > ga ? 0 : gslot_ga; };
-    float* gp = partials + (static_cast<size_t>(g) * 2 + gslot_of(g)) * B * 64 + ln;
+    float* gp = partials + (static_cast<size_t>(g) * 2 + (g > ga ? 0 : gslot_ga)) * B * 64 + ln;
 #pragma unroll
     for (int bb = 0; bb < B; ++bb)
         __hip_atomic_store(gp + bb * 64, tot[bb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the sum is complete before the count (or the barrier)
+    if (sp.defer) {
+        if (g == ga) pend = Pending{p, t, ga, gb, gslot_ga};
+        return;
+    }
     uint32_t garr = 0;
     if (ln == 0) garr = __hip_atomic_fetch_add(counters + gb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     garr = __builtin_amdgcn_readfirstlane(garr);
     if (garr != static_cast<uint32_t>(gb - ga)) return;
-    float out[B];
-#pragma unroll
-    for (int bb = 0; bb < B; ++bb) out[bb] = 0.f;
-    // loads in batches of eight, added in workgroup order
-    for (int h0 = ga; h0 <= gb; h0 += 8) {
-        float pv[8][B];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int h = h0 + u;
-            if (h <= gb) {
-                const float* ph = partials + (static_cast<size_t>(h) * 2 + gslot_of(h)) * B * 64 + ln;
-#pragma unroll
-                for (int bb = 0; bb < B; ++bb)
-                    pv[u][bb] = __hip_atomic_load(ph + bb * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (h0 + u <= gb) {
-#pragma unroll
-                for (int bb = 0; bb < B; ++bb) out[bb] += pv[u][bb];
-            }
-    }
     if (ln == 0) __hip_atomic_store(counters + gb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    store_rows<B>(P, t, out, rt);
+    combine_groups<B>(P, t, ga, gb, gslot_ga, partials);
 }
 
 // The whole launch: decoder tables staged once, then the phases in order (one
@@ -1264,14 +1305,19 @@ void gemv_kernel(const GemvChain ch) {
     int k = 0;                    // the phase
     bool live = r.live;
     bool first = true;
+    // tiles of deferred phases this wave adds up: from the phase before the
+    // last barrier (old) and from the current phase (cur)
+    Pending pend_old = no_pending(), pend_cur = no_pending();
+    const size_t pstride = static_cast<size_t>(gridDim.x) * 2 * B * 64;
+    bool abandoned = false;
     for (;;) {
         if (!Chain || live) {
             const GemvProblem& P = ch.prob[p];
             float sum[B];
             if constexpr (kMx) run_piece_mx<B>(P, pc, xp, L, xs, sum);
             else run_piece<B>(P, pc, L, sum);
-            finish_piece<B>(P, ch.ph[k], t, c, c1, first, sum, g * ch.ph[k].wpg, g, s_piece, s_cnt, counters,
-                            partials);
+            finish_piece<B>(P, ch.ph[k], p, t, c, c1, first, sum, g * ch.ph[k].wpg, g, s_piece, s_cnt, counters,
+                            partials + (Chain ? (k % ch.buffers) * pstride : 0), pend_cur);
             i += static_cast<uint32_t>(c1 - c);
             if (i < end) {
                 first = false;
@@ -1309,9 +1355,16 @@ void gemv_kernel(const GemvChain ch) {
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
             if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
+            ChainSync& cs = g_chain_sync[ch.slot];
+            if (threadIdx.x == 0) chain_arrive(cs, k - 1, g, static_cast<int>(gridDim.x));
+            // the deferred tiles of phase k - 2, complete since the barrier
+            // before phase k - 1, while this workgroup waits
+            if (pend_old.p >= 0)
+                combine_groups<B>(ch.prob[pend_old.p], pend_old.t, pend_old.ga, pend_old.gb, pend_old.gs,
+                                  partials + ((k - 2) % ch.buffers) * pstride);
+            pend_old = pend_cur;
+            pend_cur = no_pending();
             if (threadIdx.x == 0) {
-                ChainSync& cs = g_chain_sync[ch.slot];
-                chain_arrive(cs, k - 1, g, static_cast<int>(gridDim.x));
                 const bool met = chain_wait(cs, k - 1, g, ch.wait_limit);
                 if (!met) dev_add(&cs.expired[0], 1u);
                 s_cnt[2 * kGemvWaves] = met ? 0u : 1u;
@@ -1321,10 +1374,18 @@ void gemv_kernel(const GemvChain ch) {
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
             // a wait that gave up abandons the launch: running ahead could
             // overwrite piece sums that a slower workgroup has yet to read
-            if (__builtin_amdgcn_readfirstlane(s_cnt[2 * kGemvWaves])) break;
+            if (__builtin_amdgcn_readfirstlane(s_cnt[2 * kGemvWaves])) {
+                abandoned = true;
+                break;
+            }
         }
     }
     if constexpr (Chain) {
+        // the deferred tiles of the next-to-last phase (the last phase is
+        // never deferred)
+        if (!abandoned && pend_old.p >= 0)
+            combine_groups<B>(ch.prob[pend_old.p], pend_old.t, pend_old.ga, pend_old.gb, pend_old.gs,
+                              partials + ((ch.n_phases - 2) % ch.buffers) * pstride);
         // the last workgroup to finish reports the status and clears the
         // barrier words for the next launch on the slot (every workgroup has
         // passed its last wait by then)

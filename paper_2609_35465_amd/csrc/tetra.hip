@@ -228,6 +228,11 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, const int* counts, int n
                                                                  static_cast<uint32_t>(grid * ch.ph[k].wpg)));
         }
     }
+    // three partial-sum buffers for a chain when they fit in the slot (one
+    // always does: gemv_max_groups)
+    const bool rotate = n_phases > 1 && static_cast<size_t>(tetra_dev::kChainBuffers) * grid * 2 * batch * 64 <=
+                                            static_cast<size_t>(tetra_dev::kGemvSlotPartials);
+    ch.buffers = rotate ? tetra_dev::kChainBuffers : 1;
     for (int k = 0; k < n_phases; ++k) {
         tetra_dev::GemvSplit& sp = ch.ph[k];
         sp.inv_total = 1.0 / static_cast<double>(sp.total);
@@ -239,6 +244,10 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, const int* counts, int n
         for (int i = sp.p0; i < sp.p0 + sp.n; ++i) nblk_min = std::min(nblk_min, ch.prob[i].nblk);
         sp.aligned = static_cast<unsigned long long>(sp.waves) * static_cast<unsigned>(nblk_min) >= sp.total &&
                      static_cast<uint32_t>(sp.waves) <= sp.total;
+        // a chain phase other than the last adds up its tiles that span
+        // workgroups after the next barrier: tile-aligned (a wave adds up
+        // at most one tile), and with the three partial-sum buffers
+        sp.defer = rotate && k + 1 < n_phases && sp.aligned;
     }
     ch.n_phases = n_phases;
     ch.slot = slot;

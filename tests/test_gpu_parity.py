@@ -422,27 +422,54 @@ def test_chain_in_graph_replays_match_eager():
     on the same stream, give the eager launch's bits."""
     items, refs, counts = _chain_case(_CHAIN_SMALL, 1, 7500)
     probs = tt.make_problems(items)
-    tt.gemv_chain(probs, counts, 1)
+    status = torch.full((1,), 12345, dtype=torch.int32, device="cuda")
+    tt.gemv_chain(probs, counts, 1, status)
     torch.cuda.synchronize()
+    assert int(status.item()) == 0
     eager = [it[3].clone() for it in items]
     g = torch.cuda.CUDAGraph()
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
         with torch.cuda.graph(g, stream=s):
-            tt.gemv_chain(probs, counts, 1, None, s.cuda_stream)
+            tt.gemv_chain(probs, counts, 1, status, s.cuda_stream)
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     for rep in range(3):
         for it in items:
             it[3].fill_(float("nan"))
+        status.fill_(12345)
         _ = (torch.ones(1024, device="cuda") * 2).sum()     # eager work between replays
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
+        nans = [int(torch.isnan(it[3]).sum()) for it in items]
+        print(f"[chain graph] replay {rep} status {int(status.item())} NaNs per product {nans}", flush=True)
+        assert int(status.item()) == 0, rep
         for a, it in zip(eager, items):
             assert torch.equal(a, it[3]), rep
     tt.release_stream(s.cuda_stream)
+
+
+def test_chain_workspace_stays_in_its_slot():
+    """Chains at every batch class on one stream (phase sums rotating over
+    buffers where they fit, one buffer where they do not), then a chain on a
+    second stream, whose slot lies next to the first in device memory: every
+    row of the second is right (a slot overrun would have left its counters
+    nonzero and rows unwritten)."""
+    for batch in (2, 3, 4, 8, 1):
+        items, refs, counts = _chain_case(_CHAIN_SMALL, batch, 7600 + batch)
+        tt.gemv_chain(tt.make_problems(items), counts, batch)
+    torch.cuda.synchronize()
+    items, refs, counts = _chain_case(_CHAIN_SMALL, 1, 7650)
+    status = torch.full((1,), 12345, dtype=torch.int32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    tt.gemv_chain(tt.make_problems(items), counts, 1, status, s.cuda_stream)
+    torch.cuda.synchronize()
+    tt.release_stream(s.cuda_stream)
+    assert int(status.item()) == 0
+    _check_chain_outputs(items, refs, label="second slot")
 
 
 def test_chain_wait_that_gives_up_reports_and_leaves_slot_clean():
