@@ -1066,18 +1066,34 @@ __device__ __forceinline__ RowTail load_rows(const GemvProblem& P, int t) {
     return r;
 }
 
+// The tail's activation pairs are loaded four at a time (pair q read from
+// min(q, T/2 - 1), so every read is in bounds) and the pairs past the tail
+// left out by a select: a load per pair behind its own branch would cost a
+// round trip each.
 template <int B>
 __device__ __forceinline__ void store_rows(const GemvProblem& P, int t, const float (&tot)[B], const RowTail& r) {
     const int row = t * kTile + lane_now();
     if (row >= P.M) return;
     const_u32* xc = (const_u32*)(P.x);
+    const int th = P.T >> 1;                                // tail pairs
 #pragma unroll
     for (int bb = 0; bb < B; ++bb) {
         const int x0 = bb * (P.K >> 1) + 12 * P.nblk;     // first tail pair of x_b
         float ts = 0.f;
 #pragma unroll
-        for (int q = 0; q < 11; ++q)
-            if (2 * q < P.T) ts = dot2(r.tv[q], xc[x0 + q], ts);
+        for (int q0 = 0; q0 < 11; q0 += 4) {
+            if (q0 < th) {
+                uint32_t xv[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) xv[u] = xc[x0 + min(q0 + u, th - 1)];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (q0 + u < 11) {
+                        const float d = dot2(r.tv[q0 + u], xv[u], ts);
+                        ts = q0 + u < th ? d : ts;
+                    }
+            }
+        }
         P.y[static_cast<size_t>(bb) * P.M + row] = fmaf(r.sg, tot[bb], ts);
     }
 }
@@ -1091,8 +1107,57 @@ struct RangePos {
     bool live;
 };
 
-__device__ __forceinline__ RangePos range_pos(const GemvChain& ch, int k, int g, int wid) {
-    const GemvSplit& sp = ch.ph[k];
+// What a range position needs of the launch: the phase's split and the
+// first block and block columns of its problems.  Read from the kernel
+// arguments (phase 0, before anything is staged) or from the workgroup's
+// copy in LDS (later phases: the arguments' lines have long left the scalar
+// cache by then, and a chain of scalar misses would stall the wave for
+// microseconds).
+struct ArgSrc {
+    const GemvChain& ch;
+    __device__ __forceinline__ GemvSplit split(int k) const { return ch.ph[k]; }
+    __device__ __forceinline__ uint32_t base(int q) const { return ch.prob[q].blk_base; }
+    __device__ __forceinline__ int nblk(int q) const { return ch.prob[q].nblk; }
+};
+
+// the part of the kernel arguments that range positions read, staged in LDS
+struct StagedChain {
+    GemvSplit ph[kMaxPhases];
+    uint32_t base[kMaxGroup];
+    int nblk[kMaxGroup];
+};
+constexpr int kStagedWords = static_cast<int>(sizeof(StagedChain) / 4);
+static_assert(sizeof(StagedChain) % 4 == 0 && sizeof(GemvSplit) % 4 == 0, "word copies");
+
+constexpr int kSplitWords = static_cast<int>(sizeof(GemvSplit) / 4);
+
+// word w of the staged copy, from the kernel arguments
+__device__ __forceinline__ uint32_t staged_word(const GemvChain& ch, int w) {
+    if (w < kSplitWords * kMaxPhases) return reinterpret_cast<const uint32_t*>(ch.ph)[w];
+    if (w < kSplitWords * kMaxPhases + kMaxGroup) return ch.prob[w - kSplitWords * kMaxPhases].blk_base;
+    return static_cast<uint32_t>(ch.prob[min(w - kSplitWords * kMaxPhases - kMaxGroup, kMaxGroup - 1)].nblk);
+}
+
+// the staged copy, read through an LDS pointer (wave-uniform addresses; the
+// values go to scalar registers)
+struct LdsSrc {
+    lds_u32* w;
+    __device__ __forceinline__ uint32_t rd(int i) const { return __builtin_amdgcn_readfirstlane(w[i]); }
+    __device__ __forceinline__ GemvSplit split(int k) const {
+        uint32_t o[kSplitWords];
+#pragma unroll
+        for (int u = 0; u < kSplitWords; ++u) o[u] = rd(k * kSplitWords + u);
+        return __builtin_bit_cast(GemvSplit, o);
+    }
+    __device__ __forceinline__ uint32_t base(int q) const { return rd(kSplitWords * kMaxPhases + q); }
+    __device__ __forceinline__ int nblk(int q) const {
+        return static_cast<int>(rd(kSplitWords * kMaxPhases + kMaxGroup + q));
+    }
+};
+
+template <class Src>
+__device__ __forceinline__ RangePos range_pos(const Src& src, int k, int g, int wid) {
+    const GemvSplit sp = src.split(k);
     const int w = g * sp.wpg + wid;
     RangePos r;
     r.live = wid < sp.wpg && w < sp.waves;
@@ -1102,27 +1167,29 @@ __device__ __forceinline__ RangePos range_pos(const GemvChain& ch, int k, int g,
         const uint32_t bs = div_exact(static_cast<unsigned long long>(wr + 1) * sp.total - 1,
                                       static_cast<uint32_t>(sp.waves), sp.inv_waves);
         int q = sp.p0;
-        while (q + 1 < sp.p0 + sp.n && bs >= ch.prob[q + 1].blk_base) ++q;
-        const uint32_t nb = static_cast<uint32_t>(ch.prob[q].nblk);
-        const uint32_t t0 = ch.prob[q].blk_base + (bs - ch.prob[q].blk_base) / nb * nb;
+        while (q + 1 < sp.p0 + sp.n && bs >= src.base(q + 1)) ++q;
+        const uint32_t nb = static_cast<uint32_t>(src.nblk(q));
+        const uint32_t b0 = src.base(q);
+        const uint32_t t0 = b0 + (bs - b0) / nb * nb;
         const int wa = tile_first_wave(t0, sp);
         const uint32_t n = static_cast<uint32_t>(tile_first_wave(t0 + nb, sp) - wa);
         const uint32_t j = static_cast<uint32_t>(wr - wa);
         r.i = __builtin_amdgcn_readfirstlane(t0 + j * nb / n);
         r.end = __builtin_amdgcn_readfirstlane(t0 + (j + 1) * nb / n);
+        r.p = q;        // the tile's problem holds the whole range
     } else {
         r.i = __builtin_amdgcn_readfirstlane(range_begin(wr, sp));
         r.end = __builtin_amdgcn_readfirstlane(range_begin(wr + 1, sp));
+        int q = sp.p0;
+        while (q + 1 < sp.p0 + sp.n && r.i >= src.base(q + 1)) ++q;
+        r.p = q;
     }
-    int p = sp.p0;
-    while (p + 1 < sp.p0 + sp.n && r.i >= ch.prob[p + 1].blk_base) ++p;
-    r.p = p;
-    const GemvProblem& P = ch.prob[p];
-    const uint32_t rel = r.i - P.blk_base;
-    r.t = __builtin_amdgcn_readfirstlane(static_cast<int>(rel / static_cast<uint32_t>(P.nblk)));
-    r.c = __builtin_amdgcn_readfirstlane(static_cast<int>(rel - static_cast<uint32_t>(r.t) * P.nblk));
+    const int nbp = src.nblk(r.p);
+    const uint32_t rel = r.i - src.base(r.p);
+    r.t = __builtin_amdgcn_readfirstlane(static_cast<int>(rel / static_cast<uint32_t>(nbp)));
+    r.c = __builtin_amdgcn_readfirstlane(static_cast<int>(rel - static_cast<uint32_t>(r.t) * nbp));
     const uint32_t left = r.end - r.i;
-    r.c1 = left < static_cast<uint32_t>(P.nblk - r.c) ? r.c + static_cast<int>(left) : P.nblk;
+    r.c1 = left < static_cast<uint32_t>(nbp - r.c) ? r.c + static_cast<int>(left) : nbp;
     return r;
 }
 
@@ -1277,6 +1344,7 @@ void gemv_kernel(const GemvChain ch) {
     __shared__ uint32_t s_cnt[2 * kGemvWaves + 1];       // piece counts; the last word: the launch is abandoned
     constexpr bool kMx = B >= 3;
     __shared__ uint4 s_xs[kMx ? kGemvWaves * MxSets<B>::kN * kXSlotBytes / 16 : 1];   // batch >= 3: x slots per wave
+    __shared__ uint32_t s_ch[Chain ? kStagedWords : 1];   // StagedChain
     if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
     lds_bytes* L = (lds_bytes*)(s_tab);
     const int lane = threadIdx.x & 63;
@@ -1284,11 +1352,13 @@ void gemv_kernel(const GemvChain ch) {
     const int g = static_cast<int>(blockIdx.x);
     TableStage<kGemvThreads> ts;
     ts.load();
+    static_assert(kStagedWords <= kGemvThreads, "one word per thread");
+    const uint32_t chw = Chain ? staged_word(ch, min(static_cast<int>(threadIdx.x), kStagedWords - 1)) : 0u;
     uint32_t* const counters = g_gemv_slots[ch.slot].counters;
     float* const partials = g_gemv_slots[ch.slot].partials;
     // the first piece's code words are requested while the tables arrive;
     // the barrier orders LDS only, so they stay in flight across it
-    RangePos r = range_pos(ch, 0, g, wid);
+    RangePos r = range_pos(ArgSrc{ch}, 0, g, wid);
     int p = r.p, t = r.t, c = r.c, c1 = r.c1;
     uint32_t i = r.i, end = r.end;
     Piece pc = begin_piece_live(ch.prob[p], t, c, c1, lane, r.live);
@@ -1296,6 +1366,7 @@ void gemv_kernel(const GemvChain ch) {
     if constexpr (kMx) xp = begin_xpiece<B>(ch.prob[p], pc, r.live);
     uint8_t* xs = reinterpret_cast<uint8_t*>(s_xs) + (kMx ? wid * MxSets<B>::kN * kXSlotBytes : 0);
     ts.store(s_tab);
+    if (Chain && threadIdx.x < kStagedWords) s_ch[threadIdx.x] = chw;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
@@ -1338,19 +1409,11 @@ void gemv_kernel(const GemvChain ch) {
         } else {
             // the wave's range of phase k is done
             if (++k == ch.n_phases) break;
-            r = range_pos(ch, k, g, wid);
-            p = r.p;
-            t = r.t;
-            c = r.c;
-            c1 = r.c1;
-            i = r.i;
-            end = r.end;
-            live = r.live;
-            first = true;
-            pc = begin_piece_live(ch.prob[p], t, c, c1, lane, live);
-            if constexpr (kMx) xp = begin_xpiece<B>(ch.prob[p], pc, live);
             // every wave of the workgroup is done with phase k - 1 (and with its
-            // LDS pieces and counts); one lane counts the workgroup in and waits
+            // LDS pieces and counts); one lane counts the workgroup in and
+            // waits.  Meanwhile every wave adds up the deferred tiles it holds,
+            // finds its range of phase k and requests the code words of its
+            // first piece, which no phase writes.
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
@@ -1364,6 +1427,17 @@ void gemv_kernel(const GemvChain ch) {
                                   partials + ((k - 2) % ch.buffers) * pstride);
             pend_old = pend_cur;
             pend_cur = no_pending();
+            r = range_pos(LdsSrc{(lds_u32*)(s_ch)}, k, g, wid);
+            p = r.p;
+            t = r.t;
+            c = r.c;
+            c1 = r.c1;
+            i = r.i;
+            end = r.end;
+            live = r.live;
+            first = true;
+            pc = begin_piece_live(ch.prob[p], t, c, c1, lane, live);
+            if constexpr (kMx) xp = begin_xpiece<B>(ch.prob[p], pc, live);
             if (threadIdx.x == 0) {
                 const bool met = chain_wait(cs, k - 1, g, ch.wait_limit);
                 if (!met) dev_add(&cs.expired[0], 1u);
@@ -1377,6 +1451,14 @@ void gemv_kernel(const GemvChain ch) {
             if (__builtin_amdgcn_readfirstlane(s_cnt[2 * kGemvWaves])) {
                 abandoned = true;
                 break;
+            }
+            // before the last phase: the deferred tiles of phase k - 1,
+            // complete now, rather than at the launch's end, where they
+            // would add to its tail
+            if (k + 1 == ch.n_phases && pend_old.p >= 0) {
+                combine_groups<B>(ch.prob[pend_old.p], pend_old.t, pend_old.ga, pend_old.gb, pend_old.gs,
+                                  partials + ((k - 1) % ch.buffers) * pstride);
+                pend_old = no_pending();
             }
         }
     }
