@@ -405,12 +405,18 @@ inline int gemv_waves(uint32_t total, int cus, int groups) {
 // Waves per workgroup in one phase of a chain: its launch holds a whole
 // round of workgroups anyway, and the tables are staged once for all phases,
 // so a wave is worth fewer blocks than in a single launch (at least
-// kChainMinBlocks each, up to all kGemvWaves).
+// kChainMinBlocks each, up to all kGemvWaves).  A multiple of the CU's four
+// SIMDs, which take a workgroup's waves in turn: five waves would put two on
+// one SIMD and one on each of the others, and that SIMD would take twice as
+// long (measured on the 14B step: 2.44 -> 2.39 ms).
 constexpr uint32_t kChainMinBlocks = 8;
+constexpr int kSimdsPerCU = 4;
+static_assert(kGemvWaves % kSimdsPerCU == 0, "whole rounds of SIMDs");
 inline int chain_phase_wpg(uint32_t total, int groups) {
     const unsigned long long per = static_cast<unsigned long long>(kChainMinBlocks) * static_cast<uint32_t>(groups);
     const unsigned long long w = (total + per - 1) / per;
-    return static_cast<int>(w < 1 ? 1 : w > static_cast<unsigned long long>(kGemvWaves) ? kGemvWaves : w);
+    const unsigned long long w4 = (w + kSimdsPerCU - 1) / kSimdsPerCU * kSimdsPerCU;
+    return static_cast<int>(w4 > static_cast<unsigned long long>(kGemvWaves) ? kGemvWaves : w4);
 }
 
 // Partial-sum buffers of a chain whose phases defer (when three fit in the
@@ -1342,6 +1348,7 @@ void gemv_kernel(const GemvChain ch) {
     __shared__ uint4 s_tab[kPackedTableBytes / 16];
     __shared__ float s_piece[kGemvWaves * 2 * B * 64];   // [wave][first/last piece][B][64]
     __shared__ uint32_t s_cnt[2 * kGemvWaves + 1];       // piece counts; the last word: the launch is abandoned
+    constexpr int kAbandoned = 2 * kGemvWaves;
     constexpr bool kMx = B >= 3;
     __shared__ uint4 s_xs[kMx ? kGemvWaves * MxSets<B>::kN * kXSlotBytes / 16 : 1];   // batch >= 3: x slots per wave
     __shared__ uint32_t s_ch[Chain ? kStagedWords : 1];   // StagedChain
@@ -1418,15 +1425,9 @@ void gemv_kernel(const GemvChain ch) {
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
             if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
+            const bool polls = threadIdx.x == 0;    // the lane that counts the workgroup in and waits
             ChainSync& cs = g_chain_sync[ch.slot];
-            if (threadIdx.x == 0) chain_arrive(cs, k - 1, g, static_cast<int>(gridDim.x));
-            // the deferred tiles of phase k - 2, complete since the barrier
-            // before phase k - 1, while this workgroup waits
-            if (pend_old.p >= 0)
-                combine_groups<B>(ch.prob[pend_old.p], pend_old.t, pend_old.ga, pend_old.gb, pend_old.gs,
-                                  partials + ((k - 2) % ch.buffers) * pstride);
-            pend_old = pend_cur;
-            pend_cur = no_pending();
+            if (polls) chain_arrive(cs, k - 1, g, static_cast<int>(gridDim.x));
             r = range_pos(LdsSrc{(lds_u32*)(s_ch)}, k, g, wid);
             p = r.p;
             t = r.t;
@@ -1438,17 +1439,25 @@ void gemv_kernel(const GemvChain ch) {
             first = true;
             pc = begin_piece_live(ch.prob[p], t, c, c1, lane, live);
             if constexpr (kMx) xp = begin_xpiece<B>(ch.prob[p], pc, live);
-            if (threadIdx.x == 0) {
+            // the deferred tiles of phase k - 2, complete since the barrier
+            // before phase k - 1 (after the code-word requests, so that the
+            // waves waiting for those do not wait for this tile's y stores)
+            if (pend_old.p >= 0)
+                combine_groups<B>(ch.prob[pend_old.p], pend_old.t, pend_old.ga, pend_old.gb, pend_old.gs,
+                                  partials + ((k - 2) % ch.buffers) * pstride);
+            pend_old = pend_cur;
+            pend_cur = no_pending();
+            if (polls) {
                 const bool met = chain_wait(cs, k - 1, g, ch.wait_limit);
                 if (!met) dev_add(&cs.expired[0], 1u);
-                s_cnt[2 * kGemvWaves] = met ? 0u : 1u;
+                s_cnt[kAbandoned] = met ? 0u : 1u;
             }
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
             // a wait that gave up abandons the launch: running ahead could
             // overwrite piece sums that a slower workgroup has yet to read
-            if (__builtin_amdgcn_readfirstlane(s_cnt[2 * kGemvWaves])) {
+            if (__builtin_amdgcn_readfirstlane(s_cnt[kAbandoned])) {
                 abandoned = true;
                 break;
             }
