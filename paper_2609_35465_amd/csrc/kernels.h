@@ -715,6 +715,19 @@ __device__ __forceinline__ void start_pipe(Pipe<B>& st, const ItemWords& w, int 
     for (int bb = 0; bb < B; ++bb) st.pdt[bb] = 0.f;
 }
 
+// Issue priority from the share of a piece still to do (left of total
+// groups): 3 above three quarters, down to 0 below one quarter.  A SIMD
+// issues for the oldest of its ready waves first, so with equal pieces the
+// first waves of a CU would finish long before the last ones, and the last
+// ones would then run with too few waves beside them to hide their waits;
+// a wave that has fallen behind now goes first.
+__device__ __forceinline__ void progress_prio(int left, int total) {
+    if (4 * left >= 3 * total) __builtin_amdgcn_s_setprio(3);
+    else if (2 * left >= total) __builtin_amdgcn_s_setprio(2);
+    else if (4 * left >= total) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
+}
+
 // The groups alternate between two sets of word registers, so that the
 // loads of the group after next go straight into the registers just freed;
 // the trailing columns follow from their own registers.
@@ -735,17 +748,22 @@ __device__ __forceinline__ void run_piece(const GemvProblem& P, Piece& pc, lds_b
         const int kl = __builtin_amdgcn_readfirstlane(pc.tr ? tetra::kGroupCols : pc.c1 - 4 * jg);
         start_pipe<B>(st, pc.cw, kb, pc.c0, L, xc, kp);
         ItemWords wa = pc.cw, wb = pc.nw;
+        const int j0 = j, ngr = jg - j + 1;
+        __builtin_amdgcn_s_setprio(3);
         for (;;) {
             run_one_item<B>(st, kb, j == jg ? kl : tetra::kGroupCols, 4 * j, 4 * min(j + 1, jg), wa, wb, L, xc, kp);
             if (j == jg) break;
             ++j;
+            progress_prio(jg - j + 1, ngr);
             kb = 0;
             wa = load_group(tb, min(j + 1, jg), lane);
             run_one_item<B>(st, 0, j == jg ? kl : tetra::kGroupCols, 4 * j, 4 * min(j + 1, jg), wb, wa, L, xc, kp);
             if (j == jg) break;
             ++j;
+            progress_prio(jg - j + 1, ngr);
             wb = load_group(tb, min(j + 1, jg), lane);
         }
+        (void)j0;
         __builtin_amdgcn_s_waitcnt(0xC07F);
         finish_pending<B>(st);
         kb = 0;
@@ -759,6 +777,7 @@ __device__ __forceinline__ void run_piece(const GemvProblem& P, Piece& pc, lds_b
         __builtin_amdgcn_s_waitcnt(0xC07F);
         finish_pending<B>(st);
     }
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int bb = 0; bb < B; ++bb) out[bb] = st.acc[bb];
 }
