@@ -48,8 +48,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--chain-layers", type=int, default=2,
-                    help="--mode chain: layers per launch (1 or 2: a launch holds at most 16 matrices)")
+    ap.add_argument("--chain-layers", type=int, default=4,
+                    help="--mode chain: layers per launch (a launch holds at most 32 matrices and 16 phases: 4 layers)")
     ap.add_argument("--no-deps-figure", action="store_true",
                     help="--mode chain: skip timing the same step as 160 separate launches")
     ap.add_argument("--mode", default="chain", choices=["matrix", "deps", "layer", "chain"],
@@ -183,6 +183,8 @@ def build_chains(tt, plan, chain_layers, nproj=7):
         for names in GROUPS["deps"]:
             tet = [n for n in names if isinstance(by_name[n][0], Matrix)]
             i4 = [n for n in names if not isinstance(by_name[n][0], Matrix)]
+            if tet and (len(cur) + len(tet) > tt.MAX_GROUP or len(counts) == tt.MAX_PHASES):
+                flush()
             if tet:
                 cur.extend((by_name[n][0].blob, by_name[n][0].sigma, by_name[n][1], by_name[n][2],
                             by_name[n][0].M, by_name[n][0].K) for n in tet)

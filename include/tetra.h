@@ -170,7 +170,7 @@ int tetra_gemv(const void* codes, const uint16_t* row_scales, const uint16_t* x,
                float* y, int M, int K, int batch, hipStream_t stream);
 
 /* Largest number of matrices in one tetra_gemv_grouped call. */
-#define TETRA_MAX_GROUP 16
+#define TETRA_MAX_GROUP 32
 
 /* One matrix of a grouped product: arguments as in tetra_gemv. */
 typedef struct {

@@ -19,7 +19,8 @@ OK, EINVAL, EALIGN, EDEVICE, EUNSUPPORTED, EBUSY, ETIMEOUT = 0, -1, -2, -3, -4, 
 ROW_TILE = 64
 TABLE_BLOB_BYTES = 18824
 MAX_BATCH = 8
-MAX_GROUP = 16
+MAX_GROUP = 32
+MAX_PHASES = 16
 ENCODE_MAX_RADIUS = 25.0
 ENCODE_RADII = (13.0, 15.0)        # trial radii of the encoder: the best integer pair on Gaussian blocks
 

@@ -14,7 +14,7 @@ constexpr int kChunk = kTile * 6;         // bytes per (tile, block column) chun
 constexpr int kGemvWaves = 12;                 // waves per GEMV workgroup
 constexpr int kGemvThreads = kGemvWaves * 64;
 constexpr int kGemvGroupsPerCU = 2;            // at most (batch 1: 2 x 56.5 KB of LDS, 6 waves per SIMD)
-constexpr int kMaxGroup = 16;
+constexpr int kMaxGroup = 32;
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(4))) const uint32_t const_u32;

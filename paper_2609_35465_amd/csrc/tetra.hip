@@ -584,6 +584,9 @@ __global__ __launch_bounds__(256) void zero_words_kernel(uint32_t* p, int n) {
 int tetra_gemm_noalloc(const void* codes, const uint16_t* row_scales, const uint16_t* x, float* y, int M, int K,
                        int N, hipStream_t stream) {
     static_assert(tetra_dev::kChainTimeout == TETRA_ETIMEOUT, "status value written by the kernel");
+    static_assert(tetra_dev::kMaxGroup == TETRA_MAX_GROUP && tetra_dev::kMaxPhases == TETRA_MAX_PHASES,
+                  "limits of the boundary");
+    static_assert(sizeof(tetra_dev::GemvChain) <= 4096, "kernel arguments");
     static_assert(kScratchBytes >= (sizeof(uint32_t) * kScratchWorkers + 255) / 256 * 256 +
                                        sizeof(float) * static_cast<size_t>(kScratchWorkers) * 2 * tetra_dev::kPfSlot,
                   "scratch holds the counters and pieces of kScratchWorkers workgroups");

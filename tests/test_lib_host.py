@@ -209,11 +209,11 @@ def test_grouped_validation():
     fake = 0x1000
     good = tt.Problem(fake, fake, fake, fake, 64, 48)
     bad = tt.Problem(fake, fake, fake, fake, 64, 23)
-    arr = (tt.Problem * 17)(*([good] * 17))
+    arr = (tt.Problem * (tt.MAX_GROUP + 1))(*([good] * (tt.MAX_GROUP + 1)))
     p = ctypes.cast(arr, ctypes.c_void_p)
     assert lib.tetra_gemv_grouped(None, 1, 1, None) == tt.EINVAL
     assert lib.tetra_gemv_grouped(p, 0, 1, None) == tt.EINVAL
-    assert lib.tetra_gemv_grouped(p, 17, 1, None) == tt.EINVAL
+    assert lib.tetra_gemv_grouped(p, tt.MAX_GROUP + 1, 1, None) == tt.EINVAL
     assert lib.tetra_gemv_grouped(p, 2, 0, None) == tt.EINVAL
     arr2 = (tt.Problem * 2)(good, bad)
     assert lib.tetra_gemv_grouped(ctypes.cast(arr2, ctypes.c_void_p), 2, 1, None) == tt.EINVAL
