@@ -1163,11 +1163,11 @@ __device__ __forceinline__ uint32_t staged_word(const GemvChain& ch, int w) {
     return static_cast<uint32_t>(ch.prob[min(w - kSplitWords * kMaxPhases - kMaxGroup, kMaxGroup - 1)].nblk);
 }
 
-// the staged copy, read through an LDS pointer (wave-uniform addresses; the
-// values go to scalar registers)
+// the staged copy, read through an LDS pointer, one phase per lane (the
+// ranges of all later phases are worked out at once, lane k for phase k)
 struct LdsSrc {
     lds_u32* w;
-    __device__ __forceinline__ uint32_t rd(int i) const { return __builtin_amdgcn_readfirstlane(w[i]); }
+    __device__ __forceinline__ uint32_t rd(int i) const { return w[i]; }
     __device__ __forceinline__ GemvSplit split(int k) const {
         uint32_t o[kSplitWords];
 #pragma unroll
@@ -1180,8 +1180,10 @@ struct LdsSrc {
     }
 };
 
-template <class Src>
+// Uniform: k is the same on every lane (the values go to scalar registers)
+template <class Src, bool Uniform = true>
 __device__ __forceinline__ RangePos range_pos(const Src& src, int k, int g, int wid) {
+    auto rfl = [](uint32_t v) { return Uniform ? __builtin_amdgcn_readfirstlane(v) : v; };
     const GemvSplit sp = src.split(k);
     const int w = g * sp.wpg + wid;
     RangePos r;
@@ -1199,22 +1201,48 @@ __device__ __forceinline__ RangePos range_pos(const Src& src, int k, int g, int 
         const int wa = tile_first_wave(t0, sp);
         const uint32_t n = static_cast<uint32_t>(tile_first_wave(t0 + nb, sp) - wa);
         const uint32_t j = static_cast<uint32_t>(wr - wa);
-        r.i = __builtin_amdgcn_readfirstlane(t0 + j * nb / n);
-        r.end = __builtin_amdgcn_readfirstlane(t0 + (j + 1) * nb / n);
+        r.i = rfl(t0 + j * nb / n);
+        r.end = rfl(t0 + (j + 1) * nb / n);
         r.p = q;        // the tile's problem holds the whole range
     } else {
-        r.i = __builtin_amdgcn_readfirstlane(range_begin(wr, sp));
-        r.end = __builtin_amdgcn_readfirstlane(range_begin(wr + 1, sp));
+        r.i = rfl(range_begin(wr, sp));
+        r.end = rfl(range_begin(wr + 1, sp));
         int q = sp.p0;
         while (q + 1 < sp.p0 + sp.n && r.i >= src.base(q + 1)) ++q;
         r.p = q;
     }
     const int nbp = src.nblk(r.p);
     const uint32_t rel = r.i - src.base(r.p);
-    r.t = __builtin_amdgcn_readfirstlane(static_cast<int>(rel / static_cast<uint32_t>(nbp)));
-    r.c = __builtin_amdgcn_readfirstlane(static_cast<int>(rel - static_cast<uint32_t>(r.t) * nbp));
+    r.t = static_cast<int>(rfl(rel / static_cast<uint32_t>(nbp)));
+    r.c = static_cast<int>(rfl(rel - static_cast<uint32_t>(r.t) * nbp));
     const uint32_t left = r.end - r.i;
     r.c1 = left < static_cast<uint32_t>(nbp - r.c) ? r.c + static_cast<int>(left) : nbp;
+    return r;
+}
+
+// A wave's range of every later phase of a chain, worked out once (in the
+// first barrier's window) and kept in LDS, 5 words per phase: each later
+// transition reads it back instead of redoing the divisions.
+constexpr int kRangeWords = 5;
+
+__device__ __forceinline__ void put_range(uint32_t* slot, const RangePos& r) {
+    slot[0] = r.i;
+    slot[1] = r.end;
+    slot[2] = static_cast<uint32_t>(r.t);
+    slot[3] = static_cast<uint32_t>(r.c);
+    slot[4] = static_cast<uint32_t>(r.c1) | static_cast<uint32_t>(r.p) << 24 | (r.live ? 1u << 31 : 0u);
+}
+
+__device__ __forceinline__ RangePos get_range(lds_u32* slot) {
+    RangePos r;
+    r.i = __builtin_amdgcn_readfirstlane(slot[0]);
+    r.end = __builtin_amdgcn_readfirstlane(slot[1]);
+    r.t = static_cast<int>(__builtin_amdgcn_readfirstlane(slot[2]));
+    r.c = static_cast<int>(__builtin_amdgcn_readfirstlane(slot[3]));
+    const uint32_t w = __builtin_amdgcn_readfirstlane(slot[4]);
+    r.c1 = static_cast<int>(w & 0xFFFFFFu);
+    r.p = static_cast<int>((w >> 24) & 0x7Fu);
+    r.live = (w >> 31) != 0;
     return r;
 }
 
@@ -1371,6 +1399,7 @@ void gemv_kernel(const GemvChain ch) {
     constexpr bool kMx = B >= 3;
     __shared__ uint4 s_xs[kMx ? kGemvWaves * MxSets<B>::kN * kXSlotBytes / 16 : 1];   // batch >= 3: x slots per wave
     __shared__ uint32_t s_ch[Chain ? kStagedWords : 1];   // StagedChain
+    __shared__ uint32_t s_rng[Chain ? kGemvWaves * kMaxPhases * kRangeWords : 1];   // [wave][phase] ranges
     if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
     lds_bytes* L = (lds_bytes*)(s_tab);
     const int lane = threadIdx.x & 63;
@@ -1447,7 +1476,15 @@ void gemv_kernel(const GemvChain ch) {
             const bool polls = threadIdx.x == 0;    // the lane that counts the workgroup in and waits
             ChainSync& cs = g_chain_sync[ch.slot];
             if (polls) chain_arrive(cs, k - 1, g, static_cast<int>(gridDim.x));
-            r = range_pos(LdsSrc{(lds_u32*)(s_ch)}, k, g, wid);
+            // at the first barrier, lane k works out the wave's range of phase
+            // k for every later phase (only this wave reads them, and its LDS
+            // operations complete in order)
+            uint32_t* const rng = s_rng + wid * kMaxPhases * kRangeWords;
+            if (k == 1 && lane >= 1 && lane < ch.n_phases)
+                put_range(rng + lane * kRangeWords, range_pos<LdsSrc, false>(LdsSrc{(lds_u32*)(s_ch)}, lane, g, wid));
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            r = get_range((lds_u32*)(rng + k * kRangeWords));
             p = r.p;
             t = r.t;
             c = r.c;
