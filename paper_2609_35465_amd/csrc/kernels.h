@@ -298,7 +298,9 @@ struct GemvSplit {
     int wpg;                       // of them per workgroup: wave v is wave v mod wpg of workgroup v / wpg
     int p0, n;                     // its problems: prob[p0 .. p0 + n - 1]
     int aligned;                   // 1: tile-aligned split (below), 0: even split of the block sequence
-    int defer;                     // 1: tiles that span workgroups are added up after the next barrier
+    int defer;                     // tiles that span workgroups are added up after the next barrier:
+                                   // 1, their sums complete before it; 2, before the one after
+                                   // (below); 0: not deferred
 };
 
 constexpr int kMaxPhases = 16;
@@ -1370,7 +1372,14 @@ __device__ __forceinline__ void finish_piece(const GemvProblem& P, const GemvSpl
 #pragma unroll
     for (int bb = 0; bb < B; ++bb)
         __hip_atomic_store(gp + bb * 64, tot[bb], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): the sum is complete before the count (or the barrier)
+    // The sum must be complete before the count, or before the barrier after
+    // which it is read.  A wave's vector memory operations complete in the
+    // order they were issued, so a sum that is read only after the barrier
+    // that follows the next phase (defer 2) needs no wait here: the wave
+    // waits for the code words of its next piece, requested after this
+    // store, before it arrives there (a wave with no piece in that phase
+    // waits for everything before it arrives).
+    if (sp.defer != 2) __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     if (sp.defer) {
         if (g == ga) pend = Pending{p, t, ga, gb, gslot_ga};
         return;
@@ -1468,7 +1477,9 @@ void gemv_kernel(const GemvChain ch) {
             // LDS pieces and counts); one lane counts the workgroup in and
             // waits.  Meanwhile every wave adds up the deferred tiles it holds,
             // finds its range of phase k and requests the code words of its
-            // first piece, which no phase writes.
+            // first piece, which no phase writes.  A wave that had no piece in
+            // phase k - 1 may still have sums of phase k - 2 in flight.
+            if (!live) __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");

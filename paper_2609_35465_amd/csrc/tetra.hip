@@ -247,7 +247,7 @@ int launch_gemv(const tetra_gemv_problem* probs, int n, const int* counts, int n
         // a chain phase other than the last adds up its tiles that span
         // workgroups after the next barrier: tile-aligned (a wave adds up
         // at most one tile), and with the three partial-sum buffers
-        sp.defer = rotate && k + 1 < n_phases && sp.aligned;
+        sp.defer = rotate && k + 1 < n_phases && sp.aligned ? (k + 2 < n_phases ? 2 : 1) : 0;
     }
     ch.n_phases = n_phases;
     ch.slot = slot;
