@@ -5,10 +5,16 @@
 // y[n][row] = sigma_row * sum_blk s_blk * sum_j y_j x[n][24 blk + j]
 //             + sum_t tail_t x[n][24 nblk + t]
 //
-// is the same sum as the GEMV's, and it is formed the same way: the decoded
-// y_j stay exact integers in fp16, each block's 24-term products come from
-// three v_mfma_f32_32x32x8_f16 (8 k each) and are scaled by that block's
-// s_blk in fp32, sigma and the tail are applied at the end.
+// is the same sum as the GEMV's.  The decoded
+// y_j are exact integers in fp16; the block's scale is folded into them as
+// fp16(s_blk y_j), rounded once from the fp32 product, so that three
+// v_mfma_f32_32x32x8_f16 (8 k each) per block accumulate straight into the
+// sums across blocks; sigma and the tail are applied at the end.  The fold
+// costs one rounding of each weight to fp16: a relative error of at most
+// 2^-11 per weight, so at most 2^-11 (4.9e-4) of sum |w x| per output, inside
+// the 1e-3 bound of the products (the GEMV keeps the scale in fp32).  Folding
+// replaced 16 fp32 multiply-adds per block and 32-token group (64 per block
+// at four groups) by 12 conversions per block.
 //
 // MFMA roles: A = activations (32 tokens x 8 k), B = decoded weights (8 k x
 // 32 rows), D = 32 tokens x 32 rows.  Lane l holds A[l % 32][4h..4h+3] and
@@ -139,8 +145,8 @@ struct PfFetch {
     half4_t a[2][3];
 };
 
-// finish a block from its table entries: this lane's half of the values (the
-// B operand) and the block scale
+// finish a block from its table entries: this lane's half of the values
+// times the block scale (the B operand)
 __device__ __forceinline__ PfBlock pf_decode(const BlockFetch& f, int h, lds_bytes* L) {
     const uint32_t ep = f.e ^ (~f.pm & 0xFCFCFCFCu);
     const uint32_t qpair = ~f.pm & 0x3C003C00u;
@@ -163,6 +169,10 @@ __device__ __forceinline__ PfBlock pf_decode(const BlockFetch& f, int h, lds_byt
     sq += __shfl_xor(sq, 32, 64);
     const float sqb = __builtin_bit_cast(float, f.bias) + sq;
     o.s = *(lds_f32*)(L + kScaleOff + ((__builtin_bit_cast(uint32_t, sqb) >> 2) & 0x7FFu));
+#pragma unroll
+    for (int kk = 0; kk < 3; ++kk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o.b[kk][i] = static_cast<_Float16>(static_cast<float>(o.b[kk][i]) * o.s);
     return o;
 }
 
@@ -253,7 +263,7 @@ __device__ __forceinline__ void pf_stage_x(_Float16* s_x, const GemmArgs& a, int
 // 64 tokens; items are then half the size, for shapes with few rows, whose
 // items would otherwise be cut into many pieces.
 template <int TG>
-__global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
+__global__ __launch_bounds__(kPfThreads) __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(const GemmArgs a) {
     __shared__ uint4 s_tab[kPackedTableBytes / 16];
     __shared__ __attribute__((aligned(16))) _Float16 s_x[kPfTokens * kPfXStride];
     __shared__ uint32_t s_arrived;
@@ -295,39 +305,21 @@ __global__ __launch_bounds__(kPfThreads) void gemm_kernel(const GemmArgs a) {
         for (int blk = 0; blk < nb; ++blk) {
             const bool more = blk + 1 < nb;
             if (more) issue(lo[min(blk + 1, 3)], hi[min(blk + 1, 3)], blk + 1, nx);
-            float16_t p[2];
-#pragma unroll
-            for (int q = 0; q < 2; ++q) {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) p[q][e] = 0.f;
-            }
 #pragma unroll
             for (int kk = 0; kk < 3; ++kk)
 #pragma unroll
-                for (int q = 0; q < 2; ++q) p[q] = __builtin_amdgcn_mfma_f32_32x32x8f16(a01[q][kk], cur.b[kk], p[q], 0, 0, 0);
+                for (int q = 0; q < 2; ++q)
+                    acc[q] = __builtin_amdgcn_mfma_f32_32x32x8f16(a01[q][kk], cur.b[kk], acc[q], 0, 0, 0);
             half4_t a23[2][3];
             if constexpr (TG == 4) load_a(blk, 2, a23);
             PfBlock nxt;
             if (more) nxt = pf_decode(nx.f, h, L);
-#pragma unroll
-            for (int q = 0; q < 2; ++q)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) acc[q][e] = fmaf(cur.s, p[q][e], acc[q][e]);
             if constexpr (TG == 4) {
-#pragma unroll
-                for (int q = 0; q < 2; ++q) {
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) p[q][e] = 0.f;
-                }
 #pragma unroll
                 for (int kk = 0; kk < 3; ++kk)
 #pragma unroll
                     for (int q = 0; q < 2; ++q)
-                        p[q] = __builtin_amdgcn_mfma_f32_32x32x8f16(a23[q][kk], cur.b[kk], p[q], 0, 0, 0);
-#pragma unroll
-                for (int q = 0; q < 2; ++q)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) acc[2 + q][e] = fmaf(cur.s, p[q][e], acc[2 + q][e]);
+                        acc[2 + q] = __builtin_amdgcn_mfma_f32_32x32x8f16(a23[q][kk], cur.b[kk], acc[2 + q], 0, 0, 0);
             }
             if (more) {
                 cur = nxt;

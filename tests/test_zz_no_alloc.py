@@ -19,7 +19,7 @@ from paper_2609_35465_amd import workloads  # noqa: E402
 from oracle import gemv as ogemv  # noqa: E402
 
 TOL = 1e-3
-TOL_PAPER = 1e-5
+TOL_GEMM = 2.0 ** -11     # one fp16 rounding of each scaled weight (the prompt product's bound)
 
 
 def _dev(a):
@@ -56,4 +56,4 @@ def test_gemm_noalloc_matches_gemm_twice():
         worst = float((np.abs(b[:, rows].astype(np.float64) - yr) / np.maximum(norm, 1e-300)).max())
         print(f"[noalloc] worst against the oracle {worst:.3e}", flush=True)
         assert worst <= TOL
-        assert worst <= TOL_PAPER
+        assert worst <= TOL_GEMM
