@@ -406,6 +406,42 @@ def test_chain_small_every_row(batch):
         assert torch.equal(a, it[3])
 
 
+# four decode-step-like layers: the most phases and problems one launch takes
+_CHAIN_FULL = [[(300 + 7 * l, 24 * 40 + 8), (64, 24 * 40 + 8), (65, 24 * 40 + 8)] if k == 0 else
+               [(300, 24 * 12 + 2)] if k == 1 else
+               [(1000 - l, 24 * 40 + 8), (999, 24 * 40 + 8)] if k == 2 else
+               [(300 + l, 24 * 83 + 16)]
+               for l in range(4) for k in range(4)]
+
+
+@pytest.mark.parametrize("batch", [1, 3])
+def test_chain_sixteen_phases_every_row(batch):
+    """Four layers' dependency groups as one launch (16 phases, 28 products,
+    the limits of the call): the phases' sums rotate over three buffers and
+    most are added up two barriers later (batch 1 and 3), every wave's
+    ranges of phases 1-15 come from the one computation at the first
+    barrier. Every row of every product against the oracle; status 0; a
+    second launch gives the same bits."""
+    assert len(_CHAIN_FULL) == tt.MAX_PHASES
+    items, refs, counts = _chain_case(_CHAIN_FULL, batch, 7300 + batch)
+    assert len(items) <= tt.MAX_GROUP
+    status = torch.full((1,), 12345, dtype=torch.int32, device="cuda")
+    probs = tt.make_problems(items)
+    print(f"[chain 16] batch={batch} products={len(items)}", flush=True)
+    tt.gemv_chain(probs, counts, batch, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    _check_chain_outputs(items, refs, label=f"16 phases b{batch}")
+    first = [it[3].clone() for it in items]
+    for it in items:
+        it[3].fill_(float("nan"))
+    tt.gemv_chain(probs, counts, batch, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for a, it in zip(first, items):
+        assert torch.equal(a, it[3])
+
+
 @pytest.mark.parametrize("batch", [1, 4])
 def test_chain_14b_layer_every_row(batch):
     """One Qwen3-14B-shaped layer as the bench chains it ([q, k, v], [o],
