@@ -325,11 +325,15 @@ struct GemvChain {
 // streams never share one; static device memory, zero when the code object
 // loads, and every launch leaves its counters at zero again.  A slot covers
 // kGemvMaxGroups workgroups, and its partial sums [groups][2][B][64] the
-// largest batch at one workgroup per CU or batch 2 at two.
+// largest batch at one workgroup per CU or batch 2 at two; for a chain, three
+// such buffers (below) up to batch 5 at one workgroup per CU and batch 2 at
+// two (1.9 MB per slot).
 constexpr int kGemvSlots = 16;
 constexpr int kGemvMaxCUs = 320;
 constexpr int kGemvMaxGroups = kGemvMaxCUs * kGemvGroupsPerCU;
-constexpr int kGemvSlotPartials = kGemvMaxCUs * 2 * 8 * 64;
+constexpr int kGemvSlotPartials = 3 * kGemvMaxCUs * 2 * 4 * 64 > kGemvMaxCUs * 2 * 8 * 64
+                                      ? 3 * kGemvMaxCUs * 2 * 4 * 64
+                                      : kGemvMaxCUs * 2 * 8 * 64;
 
 struct GemvSlot {
     uint32_t counters[kGemvMaxGroups];
