@@ -1227,16 +1227,17 @@ __device__ __forceinline__ RangePos range_pos(const Src& src, int k, int g, int 
 }
 
 // A wave's range of every later phase of a chain, worked out once (in the
-// first barrier's window) and kept in LDS, 5 words per phase: each later
+// first barrier's window) and kept in LDS, 6 words per phase: each later
 // transition reads it back instead of redoing the divisions.
-constexpr int kRangeWords = 5;
+constexpr int kRangeWords = 6;
 
 __device__ __forceinline__ void put_range(uint32_t* slot, const RangePos& r) {
     slot[0] = r.i;
     slot[1] = r.end;
     slot[2] = static_cast<uint32_t>(r.t);
     slot[3] = static_cast<uint32_t>(r.c);
-    slot[4] = static_cast<uint32_t>(r.c1) | static_cast<uint32_t>(r.p) << 24 | (r.live ? 1u << 31 : 0u);
+    slot[4] = static_cast<uint32_t>(r.c1);
+    slot[5] = static_cast<uint32_t>(r.p) | (r.live ? 1u << 31 : 0u);
 }
 
 __device__ __forceinline__ RangePos get_range(lds_u32* slot) {
@@ -1245,9 +1246,9 @@ __device__ __forceinline__ RangePos get_range(lds_u32* slot) {
     r.end = __builtin_amdgcn_readfirstlane(slot[1]);
     r.t = static_cast<int>(__builtin_amdgcn_readfirstlane(slot[2]));
     r.c = static_cast<int>(__builtin_amdgcn_readfirstlane(slot[3]));
-    const uint32_t w = __builtin_amdgcn_readfirstlane(slot[4]);
-    r.c1 = static_cast<int>(w & 0xFFFFFFu);
-    r.p = static_cast<int>((w >> 24) & 0x7Fu);
+    r.c1 = static_cast<int>(__builtin_amdgcn_readfirstlane(slot[4]));
+    const uint32_t w = __builtin_amdgcn_readfirstlane(slot[5]);
+    r.p = static_cast<int>(w & 0x7FFFFFFFu);
     r.live = (w >> 31) != 0;
     return r;
 }
