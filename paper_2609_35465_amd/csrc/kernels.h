@@ -125,8 +125,10 @@ struct BlockFetch {
 };
 
 // lo: the 32-bit part of the word; hi: its 16-bit part in bits 0-15 (bits
-// 16-31 are ignored)
-__device__ __forceinline__ BlockFetch fetch_block(uint32_t lo, uint32_t hi, lds_bytes* L) {
+// 16-31 are ignored).  Cost: also the three rows' costs (cost, their sum of
+// U^2), one byte each.
+template <bool Cost = false>
+__device__ __forceinline__ BlockFetch fetch_block(uint32_t lo, uint32_t hi, lds_bytes* L, uint32_t* cost = nullptr) {
     const uint32_t a_path = (lo << 2) & 0x3FFCu;                      // 4 * path
     const uint32_t a1 = (lo >> 10) & 0x7FF8u;                         // 8 * phys1
     const uint32_t i2 = __builtin_amdgcn_alignbit(hi, lo, 25) & 0x7FFu;
@@ -146,6 +148,11 @@ __device__ __forceinline__ BlockFetch fetch_block(uint32_t lo, uint32_t hi, lds_
     f.r[3] = r1.y;
     f.r[4] = r2.x;
     f.r[5] = r2.y;
+    if constexpr (Cost) {
+        cost[0] = L[kCostOff + (a1 >> 3)];
+        cost[1] = L[kCostOff + (am >> 3)];
+        cost[2] = L[kCostOff + (a3 >> 3)];
+    }
     return f;
 }
 
@@ -605,8 +612,8 @@ __device__ __forceinline__ void run_item(Pipe<B>& st, const ItemWords& cw, const
 __device__ __forceinline__ ItemWords load_group(const uint8_t* tb, int j, int lane) {
     ItemWords w;
     const uint8_t* gp = tb + static_cast<size_t>(j) * tetra::kGroupBytes;
-    w.lo = *reinterpret_cast<const uint4*>(gp + 16 * lane);
-    w.hi = *reinterpret_cast<const uint2*>(gp + 1024 + 8 * lane);
+    w.lo = *reinterpret_cast<const uint4*>(gp + 16u * static_cast<uint32_t>(lane));
+    w.hi = *reinterpret_cast<const uint2*>(gp + 1024u + 8u * static_cast<uint32_t>(lane));
     return w;
 }
 
@@ -1082,6 +1089,235 @@ __device__ __forceinline__ void run_piece_mx(const GemvProblem& P, Piece& pc, co
     for (int bb = 0; bb < B; ++bb) out[bb] = *reinterpret_cast<const float*>(xs + 256 * bb + 4 * (threadIdx.x & 63));
 }
 
+// ------------------------------------------------ batch 1: matrix cores
+//
+// With q = 1 - p and s_t = (-1)^(c_t xor q) U(rho_t) (the signed row values,
+// before q is added), a block's coordinates are y_t = s_t + q, so
+//   dot(y, x) = sum s_t x_t + q sum x_t,
+//   |y|^2 = 16 m = sum s_t^2 + q (2 sum s_t + 24).
+// The products with x and the plain sums go to the matrix cores:
+// v_mfma_f32_4x4x4f16 with its A operand broadcast from one block of four
+// lanes (cbsz 4, abid b) computes, in every lane, D[r] += A_b[r] . B, where
+// A_b[r] is lane 4b + r's four values and B the lane's own.  Lanes 4c
+// (c < 6) hold chunk c of the block's activations (x_{4c..4c+3}) and lanes
+// 4c + 1 four ones; lanes 32 + 4c hold the same chunk and lanes 33 + 4c four
+// halves.  Six products with B = s (abid c) and six with B = (q, q, q, q)
+// (abid 8 + c) leave D[0] = sum (s_t + q) x_t, the block's dot product, and
+// D[1] = sum s_t + 12 q, so that 16 m = sum s_t^2 + 2 q D[1].  The vector
+// unit keeps the conversions, the signs and sum s_t^2; the twelve pk_adds of
+// q and the twelve dot products with x leave it.  All values are exact:
+// sum s_t^2, D[1] and 2^23 + 4096 g + 16 m are integers below 2^24.
+//
+// The activations of an item pass through a per-wave LDS slot: lane l loads
+// bytes 8 (l mod 24) .. +7 of the item's 192 (chunk (l mod 24) mod 6 of
+// column (l mod 24) / 6; lanes past 24 repeat them), a group ahead with the
+// item's code words, and writes them at the item's start; each block reads
+// its A operand back with one ds_read_b64 per lane.  The constants sit after
+// the four columns, repeated 48 bytes apart so that one immediate offset
+// serves every lane.
+
+constexpr int kX1Cols = 192;          // bytes of one item's activations in a slot
+constexpr int kX1Slot = 352;          // + ones and halves at kX1Cols + 48 k (+ 8), k < 4
+constexpr uint32_t kHalf2One = 0x3C003C00u, kHalf2Half = 0x38003800u;
+
+// lane l's 8 bytes of the activations of the item whose first column is
+// col0 (columns past the last one read the last column's last chunk)
+__device__ __forceinline__ uint2 load_x1(const GemvProblem& P, int col0, int m8) {
+    const uint32_t off = static_cast<uint32_t>(min(48 * col0 + m8, 48 * P.nblk - 8));
+    return *reinterpret_cast<const uint2*>(reinterpret_cast<const uint8_t*>(P.x) + off);
+}
+
+// the lane's read offset in the slot for its A operand row
+__device__ __forceinline__ int x1_read_off(int l) {
+    const int b = l >> 2, r = l & 3;
+    if (r == 0 && b < 6) return 8 * b;
+    if (r == 0 && b >= 8 && b < 14) return 8 * (b - 8);
+    return kX1Cols + (r == 1 && l >= 32 ? 8 : 0);
+}
+
+struct Pipe1 {
+    BlockFetch cur;         // its bias holds 2^23 + 4096 g + the rows' costs
+    u32x2 a;                // the current block's A operand
+    float ps, pdt, acc;
+};
+
+// chunk C of a block (coordinates 4C..4C+3): its signed values into the
+// product, and its four q's (abid 8 + C; independent of the values, so the
+// two products need no wait between them beyond the conversions)
+template <int C>
+__device__ __forceinline__ void chunk_products(const BlockFetch& f, uint32_t ep, half4_t A, half4_t Q, f32x4& d) {
+    const uint32_t sg = f.r[C] ^ ((ep << C) & 0x80808080u);
+    const uint32_t s0 = cvt_pair<false>(sg), s1 = cvt_pair<true>(sg);
+    d = __builtin_amdgcn_mfma_f32_4x4x4f16(A, Q, d, 4, 8 + C, 0);
+    d = __builtin_amdgcn_mfma_f32_4x4x4f16(A, as_half4(s0, s1), d, 4, C, 0);
+}
+
+// D[0] = the block's dot product, D[1] = sum s_t + 12 q
+__device__ __forceinline__ f32x4 block_products1(const BlockFetch& f, u32x2 a) {
+    const uint32_t ep = f.e ^ (~f.pm & 0xFCFCFCFCu);
+    const uint32_t qp = ~f.pm & kHalf2One;
+    const half4_t A = as_half4(a.x, a.y), Q = as_half4(qp, qp);
+    f32x4 d = {0.f, 0.f, 0.f, 0.f};
+    chunk_products<0>(f, ep, A, Q, d);
+    chunk_products<1>(f, ep, A, Q, d);
+    chunk_products<2>(f, ep, A, Q, d);
+    chunk_products<3>(f, ep, A, Q, d);
+    chunk_products<4>(f, ep, A, Q, d);
+    chunk_products<5>(f, ep, A, Q, d);
+    return d;
+}
+
+// 2^23 + 4096 g + 16 m from the bias with the row costs (sum s_t^2) and
+// D[1]: 16 m = sum s_t^2 + 2 q (sum s_t + 12)
+__device__ __forceinline__ float block_norm1(const BlockFetch& f, float d1) {
+    return fmaf(__builtin_bit_cast(float, ~f.pm & 0x40000000u), d1, __builtin_bit_cast(float, f.bias));
+}
+
+typedef __attribute__((address_space(3))) uint8_t lds_bytes_w;
+typedef __attribute__((address_space(3))) u32x2 lds_u2_w;
+
+__device__ __forceinline__ void put_x1(lds_bytes_w* xs, int m8, uint2 xw) {
+    *(lds_u2_w*)(xs + m8) = u32x2{xw.x, xw.y};
+}
+
+// Blocks kb..ke-1 of one item (words cw; the next item's words nw and
+// activations xn), as run_item.  Each block reads the next block's A operand
+// with its table rows; the last one first writes the next item's
+// activations to the slot (every read of this item's was issued before, and
+// a wave's LDS operations complete in order).  xs: the wave's slot, m8 =
+// 8 (lane mod 24), ro: x1_read_off.
+template <bool Full>
+__device__ __forceinline__ void run_item1(Pipe1& st, const ItemWords& cw, const ItemWords& nw, uint2 xn, int kb,
+                                          int ke, lds_bytes* L, lds_bytes_w* xs, int m8, int ro) {
+#pragma unroll
+    for (int k = 0; k < tetra::kGroupCols; ++k) {
+        if (Full || (k >= kb && k < ke)) {
+            uint32_t lo, hi;
+            int an;
+            if (k + 1 < tetra::kGroupCols && (Full || k + 1 < ke)) {
+                if (k == 0) block_word<1>(cw, lo, hi);
+                else if (k == 1) block_word<2>(cw, lo, hi);
+                else block_word<3>(cw, lo, hi);
+                an = 48 * (k + 1);
+            } else {
+                block_word<0>(nw, lo, hi);
+                put_x1(xs, m8, xn);
+                an = 0;
+            }
+            const f32x4 d = block_products1(st.cur, st.a);
+            __builtin_amdgcn_sched_barrier(0);
+            uint32_t cn[3];
+            BlockFetch nxt = fetch_block<true>(lo, hi, L, cn);
+            const u32x2 a = *(lds_u2*)(xs + ro + an);
+            const float sq = block_norm1(st.cur, d[1]);
+            __builtin_amdgcn_sched_barrier(0);
+            // one wait per block: the next block's reads and the previous
+            // block's scale
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            st.acc = fmaf(st.ps, st.pdt, st.acc);
+            const uint32_t sa = (__builtin_bit_cast(uint32_t, sq) >> 2) & 0x7FFu;
+            st.ps = *(lds_f32*)(L + kScaleOff + sa);
+            st.pdt = d[0];
+            asm volatile("" : : "v"(st.pdt));
+            __builtin_amdgcn_sched_barrier(0);
+            nxt.bias += cn[0] + cn[1] + cn[2];
+            st.cur = nxt;
+            st.a = a;
+        }
+    }
+}
+
+__device__ __forceinline__ void run_one_item1(Pipe1& st, int kb, int ke, const ItemWords& cw, const ItemWords& nw,
+                                              uint2 xn, lds_bytes* L, lds_bytes_w* xs, int m8, int ro) {
+    if (kb == 0 && ke == tetra::kGroupCols)
+        run_item1<true>(st, cw, nw, xn, 0, tetra::kGroupCols, L, xs, m8, ro);
+    else
+        run_item1<false>(st, cw, nw, xn, kb, ke, L, xs, m8, ro);
+}
+
+// first block of a run of items: the item's activations into the slot, the
+// block's table reads and A operand, and an empty "previous block"
+__device__ __forceinline__ void start_pipe1(Pipe1& st, const ItemWords& w, uint2 xw, int kb, lds_bytes* L,
+                                            lds_bytes_w* xs, int m8, int ro) {
+    uint32_t lo, hi;
+    if (kb == 0) block_word<0>(w, lo, hi);
+    else if (kb == 1) block_word<1>(w, lo, hi);
+    else if (kb == 2) block_word<2>(w, lo, hi);
+    else block_word<3>(w, lo, hi);
+    put_x1(xs, m8, xw);
+    uint32_t cn[3];
+    st.cur = fetch_block<true>(lo, hi, L, cn);
+    st.a = *(lds_u2*)(xs + ro + 48 * kb);
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    st.cur.bias += cn[0] + cn[1] + cn[2];
+    st.ps = 0.f;
+    st.pdt = 0.f;
+}
+
+// run_piece at batch 1.  The activations of an item are requested one item
+// ahead, before the item's code words (so that waiting for them never waits
+// for later words); after the last group they are those of the trailing
+// columns, the item that follows it.  They are requested here, after the
+// chain barrier: the piece's code words may have been requested before it.
+__device__ __forceinline__ void run_piece1(const GemvProblem& P, Piece& pc, lds_bytes* L, lds_bytes_w* xs,
+                                           float (&out)[1]) {
+    const int lane = threadIdx.x & 63;
+    const int m8 = 8 * (lane % 24);
+    const int ro = x1_read_off(lane);
+    const uint8_t* tb = P.codes + static_cast<size_t>(pc.t) * P.nblk * kChunk;
+    const int jg = pc.jg;
+    int j = pc.j;
+    int kb = pc.c0 - 4 * j;
+    Pipe1 st;
+    st.acc = 0.f;
+    uint2 xn = load_x1(P, 4 * j, m8);      // item j, or the trailing columns when j > jg
+    if (j <= jg) {
+        const int kl = __builtin_amdgcn_readfirstlane(pc.tr ? tetra::kGroupCols : pc.c1 - 4 * jg);
+        ItemWords wa = pc.cw, wb = pc.nw;
+        const uint2 xw = xn;
+        xn = load_x1(P, 4 * (j + 1), m8);
+        start_pipe1(st, wa, xw, kb, L, xs, m8, ro);
+        const int ngr = jg - j + 1;
+        __builtin_amdgcn_s_setprio(3);
+        for (;;) {
+            run_one_item1(st, kb, j == jg ? kl : tetra::kGroupCols, wa, wb, xn, L, xs, m8, ro);
+            if (j == jg) break;
+            ++j;
+            progress_prio(jg - j + 1, ngr);
+            kb = 0;
+            xn = load_x1(P, 4 * (j + 1), m8);
+            wa = load_group(tb, min(j + 1, jg), lane);
+            run_one_item1(st, 0, j == jg ? kl : tetra::kGroupCols, wb, wa, xn, L, xs, m8, ro);
+            if (j == jg) break;
+            ++j;
+            progress_prio(jg - j + 1, ngr);
+            xn = load_x1(P, 4 * (j + 1), m8);
+            wb = load_group(tb, min(j + 1, jg), lane);
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        st.acc = fmaf(st.ps, st.pdt, st.acc);
+        kb = 0;
+    }
+    if (pc.tr) {
+        ItemWords tw = pc.tw;
+        trailing_fixup(tw, P.rem);
+        start_pipe1(st, tw, xn, kb, L, xs, m8, ro);
+        run_item1<false>(st, tw, tw, xn, kb, pc.c1 - 4 * P.ng, L, xs, m8, ro);
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        st.acc = fmaf(st.ps, st.pdt, st.acc);
+    }
+    __builtin_amdgcn_s_setprio(1);
+    out[0] = st.acc;
+}
+
+// the constants of a wave's slot (lanes 0-7: ones, halves of item column k)
+__device__ __forceinline__ void x1_slot_init(lds_bytes_w* xs) {
+    const int l = threadIdx.x & 63;
+    const uint32_t v = (l & 1) ? kHalf2Half : kHalf2One;
+    if (l < 8) *(lds_u2_w*)(xs + kX1Cols + 48 * (l >> 1) + 8 * (l & 1)) = u32x2{v, v};
+}
+
+
 // y of a tile's rows: sigma_row * sum + unquantised tail (T = K mod 24 is
 // even, so the tail is at most 11 fp16 pairs).  load_rows issues the loads,
 // store_rows does the arithmetic and the stores, so that the loads can be in
@@ -1417,6 +1653,8 @@ void gemv_kernel(const GemvChain ch) {
     constexpr int kAbandoned = 2 * kGemvWaves;
     constexpr bool kMx = B >= 3;
     __shared__ uint4 s_xs[kMx ? kGemvWaves * MxSets<B>::kN * kXSlotBytes / 16 : 1];   // batch >= 3: x slots per wave
+    constexpr bool kX1 = B == 1;
+    __shared__ uint2 s_x1[kX1 ? kGemvWaves * kX1Slot / 8 : 1];                         // batch 1: x slots per wave
     __shared__ uint32_t s_ch[Chain ? kStagedWords : 1];   // StagedChain
     __shared__ uint32_t s_rng[Chain ? kGemvWaves * kMaxPhases * kRangeWords : 1];   // [wave][phase] ranges
     if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
@@ -1436,6 +1674,8 @@ void gemv_kernel(const GemvChain ch) {
     int p = r.p, t = r.t, c = r.c, c1 = r.c1;
     uint32_t i = r.i, end = r.end;
     Piece pc = begin_piece_live(ch.prob[p], t, c, c1, lane, r.live);
+    lds_bytes_w* const x1s = (lds_bytes_w*)(s_x1) + (kX1 ? wid * kX1Slot : 0);
+    if constexpr (kX1) x1_slot_init(x1s);
     XGroup<B> xp;
     if constexpr (kMx) xp = begin_xpiece<B>(ch.prob[p], pc, r.live);
     uint8_t* xs = reinterpret_cast<uint8_t*>(s_xs) + (kMx ? wid * MxSets<B>::kN * kXSlotBytes : 0);
@@ -1460,6 +1700,7 @@ void gemv_kernel(const GemvChain ch) {
             const GemvProblem& P = ch.prob[p];
             float sum[B];
             if constexpr (kMx) run_piece_mx<B>(P, pc, xp, L, xs, sum);
+            else if constexpr (kX1) run_piece1(P, pc, L, x1s, sum);
             else run_piece<B>(P, pc, L, sum);
             finish_piece<B>(P, ch.ph[k], p, t, c, c1, first, sum, g * ch.ph[k].wpg, g, s_piece, s_cnt, counters,
                             partials + (Chain ? (k % ch.buffers) * pstride : 0), pend_cur);
@@ -1493,7 +1734,12 @@ void gemv_kernel(const GemvChain ch) {
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-            if (threadIdx.x < 2 * kGemvWaves) s_cnt[threadIdx.x] = 0;
+            {
+                // the thread index from the lane at hand: an address kept
+                // from the launch's start would hold a register throughout
+                const int tx = wid * 64 + lane_now();
+                if (tx < 2 * kGemvWaves) s_cnt[tx] = 0;
+            }
             const bool polls = threadIdx.x == 0;    // the lane that counts the workgroup in and waits
             ChainSync& cs = g_chain_sync[ch.slot];
             if (polls) chain_arrive(cs, k - 1, g, static_cast<int>(gridDim.x));

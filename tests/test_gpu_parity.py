@@ -239,12 +239,17 @@ def test_gemv_batches(batch):
     x = workloads.activations(500 + batch, batch, K)
     yb = _check_gemv(pk, x, label="batch")
     # a launch this small has fewer waves than one round of workgroups at
-    # every batch, so it splits alike; batches 1-2 take the VALU dot product
-    # and 3-8 the matrix cores, so each row equals, bit for bit, the row of
-    # the same activation in a call of the smallest batch of its class
-    for b in range(batch):
-        if batch <= 2:
-            ref = pk.gemv(x[b:b + 1])[0]
+    # every batch, so it splits alike.  The dot products take three routes:
+    # batch 1 the matrix cores with the activations broadcast, batch 2 the
+    # VALU, batches 3-8 the matrix cores with the rows in quads; within a
+    # class each row equals, bit for bit, the row of the same activation in
+    # a call of the smallest batch of the class (row b of batch 2 is row 1 of
+    # [x_b, x_b])
+    for b in range(1 if batch == 1 else batch):
+        if batch == 1:
+            ref = pk.gemv(x)[0]
+        elif batch == 2:
+            ref = pk.gemv(np.repeat(x[b:b + 1], 2, axis=0))[1]
         else:
             ref = pk.gemv(np.repeat(x[b:b + 1], 3, axis=0))[1]
         assert np.array_equal(ref, yb[b])
@@ -252,16 +257,16 @@ def test_gemv_batches(batch):
 
 def test_gemv_batch_classes_on_a_full_launch():
     """27,264 blocks: the wave count is one round of resident workgroups,
-    which on MI355X differs between batch 1-2 (VALU dot product, two
-    workgroups per CU) and batch 3-8 (matrix cores, one).  Within a class a
-    row is bit for bit the row of the same activation at another batch;
-    every batch is within the parity bound of the oracle."""
+    which on MI355X differs between batch 1-2 (two workgroups per CU) and
+    batch 3-8 (one).  Within the class of batches 3-8 a row is bit for bit
+    the row of the same activation at another batch; every batch is within
+    the parity bound of the oracle."""
     M, K = 8192, 24 * 213 + 8
     words, sigma, tail = workloads.tetra_matrix(77, M, K)
     pk = Packed(words, sigma, tail, K)
     x = workloads.activations(77, 8, K)
     y = {b: pk.gemv(x[:b]) for b in (1, 2, 3, 4, 8)}
-    assert np.array_equal(y[2][0], y[1][0])
+    assert np.array_equal(pk.gemv(np.repeat(x[1:2], 2, axis=0))[1], y[2][1])
     for b in (4, 8):
         assert np.array_equal(y[b][:3], y[3])
     rows = _sample_rows(M, np.random.default_rng(77))
