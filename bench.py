@@ -23,6 +23,7 @@ Prints one JSON line (rank 0, N = 1):
 """
 
 import argparse
+import re
 import json
 import os
 import sys
@@ -390,19 +391,36 @@ LAUNCH_SOURCE = "paper_2609_35465_amd/csrc/tetra.hip"
 TRAFFIC_PROFILE = "profiles/gemv_kernel_qwen3-14b-40-layers_traffic.md"
 
 
+def _code_only(text):
+    """C++ source without its comments and blank lines, trailing spaces
+    stripped: a change to a comment leaves the hash below as it was."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    out = []
+    for line in text.split("\n"):
+        i = line.find("//")
+        while i >= 0 and line.count('"', 0, i) % 2 == 1:     # inside a string literal
+            i = line.find("//", i + 2)
+        if i >= 0:
+            line = line[:i]
+        line = line.rstrip()
+        if line:
+            out.append(line)
+    return "\n".join(out)
+
+
 def kernel_source_hash():
     """sha256 over what decides the measured kernel: the device sources of the
     GEMV, its launch planning (the `launch_gemv` function of the library) and
-    the compiler flags."""
+    the compiler flags, comments left out."""
     import hashlib
     from paper_2609_35465_amd import build as _build
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        h.update(open(os.path.join(ROOT, f), "rb").read())
+        h.update(_code_only(open(os.path.join(ROOT, f), encoding="utf-8").read()).encode())
     lines = open(os.path.join(ROOT, LAUNCH_SOURCE), encoding="utf-8").read().split("\n")
     start = next(i for i, l in enumerate(lines) if l.startswith("int launch_gemv("))
     end = next(i for i in range(start, len(lines)) if lines[i] == "}")
-    h.update("\n".join(lines[start:end + 1]).encode())
+    h.update(_code_only("\n".join(lines[start:end + 1])).encode())
     h.update(" ".join(_build.HIP_FLAGS).encode())
     return h.hexdigest()
 

@@ -1103,18 +1103,20 @@ __device__ __forceinline__ void run_piece_mx(const GemvProblem& P, Piece& pc, co
 // 4c + 1 four ones; lanes 32 + 4c hold the same chunk and lanes 33 + 4c four
 // halves.  Six products with B = s (abid c) and six with B = (q, q, q, q)
 // (abid 8 + c) leave D[0] = sum (s_t + q) x_t, the block's dot product, and
-// D[1] = sum s_t + 12 q, so that 16 m = sum s_t^2 + 2 q D[1].  The vector
-// unit keeps the conversions, the signs and sum s_t^2; the twelve pk_adds of
-// q and the twelve dot products with x leave it.  All values are exact:
-// sum s_t^2, D[1] and 2^23 + 4096 g + 16 m are integers below 2^24.
+// D[1] = sum s_t + 12 q, so that 16 m = sum s_t^2 + 2 q D[1].  sum s_t^2
+// does not depend on the signs: it is the three rows' stored costs (sum of
+// U^2 over a row).  The vector unit keeps the conversions and the signs; the
+// pk_adds of q, the dot products with x and the norm's squares leave it.
+// All values on the norm's path are exact: sum s_t^2, D[1] and 2^23 + 4096 g
+// + 16 m are integers below 2^24.
 //
 // The activations of an item pass through a per-wave LDS slot: lane l loads
 // bytes 8 (l mod 24) .. +7 of the item's 192 (chunk (l mod 24) mod 6 of
-// column (l mod 24) / 6; lanes past 24 repeat them), a group ahead with the
-// item's code words, and writes them at the item's start; each block reads
-// its A operand back with one ds_read_b64 per lane.  The constants sit after
-// the four columns, repeated 48 bytes apart so that one immediate offset
-// serves every lane.
+// column (l mod 24) / 6; lanes past 24 repeat them) one item ahead, and the
+// previous item's last block writes them to the slot; each block reads the
+// next block's A operand with one ds_read_b64 per lane.  The constants sit
+// after the four columns, repeated 48 bytes apart so that one immediate
+// offset serves every lane.
 
 constexpr int kX1Cols = 192;          // bytes of one item's activations in a slot
 constexpr int kX1Slot = 352;          // + ones and halves at kX1Cols + 48 k (+ 8), k < 4

@@ -266,3 +266,12 @@ def test_int4_head4_and_emb4_validation():
     assert lib.tetra_encode(fake + 2, fake, 4, 14.0, 17.0, fake, None) == tt.EALIGN
     assert lib.tetra_encode(fake, fake, 4, 14.0, 17.0, fake + 1, None) == tt.EALIGN
 
+
+
+def test_kernel_hash_ignores_comments_only():
+    """The traffic record's source hash covers code, not comments: stripping
+    comments keeps every code line and drops comment-only text."""
+    import bench
+    src = 'int a = 1; // one\n/* block\n comment */ int b = 2;\n  \nasm("s // t"); // x\n'
+    assert bench._code_only(src) == 'int a = 1;\n int b = 2;\nasm("s // t");'
+    assert bench._code_only(src) != bench._code_only(src.replace("2;", "3;"))
