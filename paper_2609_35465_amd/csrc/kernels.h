@@ -349,23 +349,24 @@ struct GemvSlot {
 
 __device__ GemvSlot g_gemv_slots[kGemvSlots];
 
-// Words of the chain barrier of a slot, each on its own 128-byte line.  The
-// workgroups of a launch form kBarrierGroups groups (blockIdx mod 16); a
-// workgroup done with phase k counts itself into its group, the last of a
-// group counts the group into `count`, and the last group raises every
-// group's flag to k + 1, which the group's workgroups poll.  Spreading the
-// arrivals over several counters keeps them from queueing on one address
-// (measured with 512 workgroups: one counter for all makes the decode step
-// 15 % slower; 4, 8, 16 and 32 groups: 2.239, 2.231, 2.226 and 2.268 ms).
-// All words are touched only with device-scope atomics.  Counts and flags
-// grow within a launch; the last workgroup to finish the launch puts them
-// back to zero.
+// Words of the chain barrier of a slot.  The workgroups of a launch form
+// kBarrierGroups groups (blockIdx mod 16); a workgroup done with phase k
+// counts itself into its group's counter (a 128-byte line of its own), and
+// the last of a group writes k + 1 into word q of every group's arrival
+// line, where q is its group.  A group's workgroups poll their own arrival
+// line with one vector load (a lane per word) until every group's word
+// reads k + 1: the barrier's critical path is one atomic round trip, the
+// stores and one poll, with no second-level counter between them.
+// Spreading the arrivals over several counters keeps them from queueing on
+// one address (with 512 workgroups, one counter for all made the decode
+// step 15-18 % slower).  All words are touched only with device-scope
+// atomics.  Counts and arrival words grow within a launch; the last
+// workgroup to finish the launch puts them back to zero.
 constexpr int kBarrierGroups = 16;
 static_assert((kBarrierGroups & (kBarrierGroups - 1)) == 0, "a power of two");
 struct ChainSync {
     uint32_t grp[kBarrierGroups][32];
-    uint32_t count[32];
-    uint32_t flag[kBarrierGroups][32];
+    uint32_t arrived[kBarrierGroups][32];   // line h: word q = phases group q has finished
     uint32_t exit[32];             // workgroups finished
     uint32_t expired[32];          // waits that gave up
 };
@@ -390,20 +391,23 @@ __device__ __forceinline__ void chain_arrive(ChainSync& cs, int k, int wg, int n
     const uint32_t per = static_cast<uint32_t>(nwg) / G + (static_cast<uint32_t>(nwg) % G > q ? 1u : 0u);
     const uint32_t target = static_cast<uint32_t>(k) + 1u;
     if (dev_add(&cs.grp[q][0], 1u) + 1u == target * per)
-        if (dev_add(&cs.count[0], 1u) + 1u == target * groups)
-            for (uint32_t h = 0; h < groups; ++h) dev_store(&cs.flag[h][0], target);
+        for (uint32_t h = 0; h < groups; ++h) dev_store(&cs.arrived[h][q], target);
 }
 
 // waits until every workgroup is done with phase k; false when it gave up
-// after `limit` polls
-__device__ __forceinline__ bool chain_wait(const ChainSync& cs, int k, int wg, uint32_t limit) {
+// after `limit` polls.  Run by all 64 lanes of one wave: lane l reads word
+// l mod groups of the workgroup's arrival line.
+__device__ __forceinline__ bool chain_wait(const ChainSync& cs, int k, int wg, int nwg, uint32_t limit) {
     const uint32_t q = static_cast<uint32_t>(wg) % kBarrierGroups;
+    const uint32_t groups = static_cast<uint32_t>(nwg) < kBarrierGroups ? static_cast<uint32_t>(nwg) : kBarrierGroups;
+    const uint32_t h = static_cast<uint32_t>(lane_now()) % groups;
     const uint32_t target = static_cast<uint32_t>(k) + 1u;
-    for (uint32_t n = 0; dev_load(&cs.flag[q][0]) < target;) {
+    for (uint32_t n = 0;;) {
+        const bool behind = dev_load(&cs.arrived[q][h]) < target;
+        if (__builtin_amdgcn_ballot_w64(behind) == 0) return true;
         __builtin_amdgcn_s_sleep(1);
         if (++n > limit) return false;
     }
-    return true;
 }
 
 // wave count of a single-phase launch: one round of the 768-thread
@@ -1772,10 +1776,12 @@ void gemv_kernel(const GemvChain ch) {
                                   partials + ((k - 2) % ch.buffers) * pstride);
             pend_old = pend_cur;
             pend_cur = no_pending();
-            if (polls) {
-                const bool met = chain_wait(cs, k - 1, g, ch.wait_limit);
-                if (!met) dev_add(&cs.expired[0], 1u);
-                s_cnt[kAbandoned] = met ? 0u : 1u;
+            if (wid == 0) {
+                const bool met = chain_wait(cs, k - 1, g, static_cast<int>(gridDim.x), ch.wait_limit);
+                if (polls) {
+                    if (!met) dev_add(&cs.expired[0], 1u);
+                    s_cnt[kAbandoned] = met ? 0u : 1u;
+                }
             }
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
             __builtin_amdgcn_s_barrier();
@@ -1813,9 +1819,8 @@ void gemv_kernel(const GemvChain ch) {
                                    __HIP_MEMORY_SCOPE_AGENT);
             for (int h = 0; h < kBarrierGroups; ++h) {
                 dev_store(&cs.grp[h][0], 0u);
-                dev_store(&cs.flag[h][0], 0u);
+                for (int q = 0; q < kBarrierGroups; ++q) dev_store(&cs.arrived[h][q], 0u);
             }
-            dev_store(&cs.count[0], 0u);
             // an abandoned launch may leave tiles half counted
             if (gave_up)
                 for (uint32_t h = 0; h < gridDim.x; ++h) dev_store(counters + h, 0u);
