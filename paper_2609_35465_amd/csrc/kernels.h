@@ -350,7 +350,7 @@ struct GemvSlot {
 __device__ GemvSlot g_gemv_slots[kGemvSlots];
 
 // Words of the chain barrier of a slot.  The workgroups of a launch form
-// kBarrierGroups groups (blockIdx mod 16); a workgroup done with phase k
+// kBarrierGroups groups (blockIdx mod 8); a workgroup done with phase k
 // counts itself into its group's counter (a 128-byte line of its own), and
 // the last of a group writes k + 1 into word q of every group's arrival
 // line, where q is its group.  A group's workgroups poll their own arrival
@@ -359,10 +359,12 @@ __device__ GemvSlot g_gemv_slots[kGemvSlots];
 // stores and one poll, with no second-level counter between them.
 // Spreading the arrivals over several counters keeps them from queueing on
 // one address (with 512 workgroups, one counter for all made the decode
-// step 15-18 % slower).  All words are touched only with device-scope
-// atomics.  Counts and arrival words grow within a launch; the last
-// workgroup to finish the launch puts them back to zero.
-constexpr int kBarrierGroups = 16;
+// step 15-18 % slower; 4, 8, 16 and 32 groups: 1.949-1.960, 1.950-1.969,
+// 1.970-1.974 and 2.12 ms, the last with a whole line per poll).  All
+// words are touched only with device-scope atomics.  Counts and arrival
+// words grow within a launch; the last workgroup to finish the launch puts
+// them back to zero.
+constexpr int kBarrierGroups = 8;
 static_assert((kBarrierGroups & (kBarrierGroups - 1)) == 0, "a power of two");
 struct ChainSync {
     uint32_t grp[kBarrierGroups][32];
