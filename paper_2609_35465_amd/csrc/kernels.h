@@ -398,11 +398,12 @@ __device__ __forceinline__ void chain_arrive(ChainSync& cs, int k, int wg, int n
 
 // waits until every workgroup is done with phase k; false when it gave up
 // after `limit` polls.  Run by all 64 lanes of one wave: lane l reads word
-// l mod groups of the workgroup's arrival line.
+// l mod kBarrierGroups of the workgroup's arrival line (word 0 past the
+// launch's groups).
 __device__ __forceinline__ bool chain_wait(const ChainSync& cs, int k, int wg, int nwg, uint32_t limit) {
     const uint32_t q = static_cast<uint32_t>(wg) % kBarrierGroups;
-    const uint32_t groups = static_cast<uint32_t>(nwg) < kBarrierGroups ? static_cast<uint32_t>(nwg) : kBarrierGroups;
-    const uint32_t h = static_cast<uint32_t>(lane_now()) % groups;
+    const uint32_t l = static_cast<uint32_t>(lane_now()) & (kBarrierGroups - 1);
+    const uint32_t h = l < static_cast<uint32_t>(nwg) ? l : 0u;
     const uint32_t target = static_cast<uint32_t>(k) + 1u;
     for (uint32_t n = 0;;) {
         const bool behind = dev_load(&cs.arrived[q][h]) < target;
@@ -1755,8 +1756,13 @@ void gemv_kernel(const GemvChain ch) {
             // k for every later phase (only this wave reads them, and its LDS
             // operations complete in order)
             uint32_t* const rng = s_rng + wid * kMaxPhases * kRangeWords;
-            if (k == 1 && lane >= 1 && lane < ch.n_phases)
-                put_range(rng + lane * kRangeWords, range_pos<LdsSrc, false>(LdsSrc{(lds_u32*)(s_ch)}, lane, g, wid));
+            if (k == 1) {
+                // the lane index afresh: an address kept from the launch's
+                // start would hold a register throughout
+                const int ln = lane_now();
+                if (ln >= 1 && ln < ch.n_phases)
+                    put_range(rng + ln * kRangeWords, range_pos<LdsSrc, false>(LdsSrc{(lds_u32*)(s_ch)}, ln, g, wid));
+            }
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
             r = get_range((lds_u32*)(rng + k * kRangeWords));
