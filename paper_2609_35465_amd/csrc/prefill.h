@@ -14,7 +14,11 @@
 // 2^-11 per weight, so at most 2^-11 (4.9e-4) of sum |w x| per output, inside
 // the 1e-3 bound of the products (the GEMV keeps the scale in fp32).  Folding
 // replaced 16 fp32 multiply-adds per block and 32-token group (64 per block
-// at four groups) by 12 conversions per block.
+// at four groups) by the fold's mixed-precision fmas (v_fma_mix: an fp16
+// value times the fp32 scale, rounded once to fp16): 12 per block, against
+// 30 for the conversions, multiplies and packs of a plain fp32 product.  The
+// product is bound by latency, not issue: 82 -> 64 VALU instructions per
+// block and wave left its time unchanged (250-253 TFLOP/s).
 //
 // MFMA roles: A = activations (32 tokens x 8 k), B = decoded weights (8 k x
 // 32 rows), D = 32 tokens x 32 rows.  Lane l holds A[l % 32][4h..4h+3] and
@@ -172,7 +176,7 @@ __device__ __forceinline__ PfBlock pf_decode(const BlockFetch& f, int h, lds_byt
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) o.b[kk][i] = static_cast<_Float16>(static_cast<float>(o.b[kk][i]) * o.s);
+        for (int i = 0; i < 4; ++i) o.b[kk][i] = static_cast<_Float16>(__builtin_fmaf(static_cast<float>(o.b[kk][i]), o.s, 0.0f));
     return o;
 }
 
