@@ -130,9 +130,22 @@ struct BlockFetch {
 template <bool Cost = false>
 __device__ __forceinline__ BlockFetch fetch_block(uint32_t lo, uint32_t hi, lds_bytes* L, uint32_t* cost = nullptr) {
     const uint32_t a_path = (lo << 2) & 0x3FFCu;                      // 4 * path
-    const uint32_t a1 = (lo >> 10) & 0x7FF8u;                         // 8 * phys1
-    const uint32_t i2 = __builtin_amdgcn_alignbit(hi, lo, 25) & 0x7FFu;
-    const uint32_t am = i2 * 8u + 8u * tetra::kMidOffset;             // 8 * (808 + i2), bit 14 = delta
+    // i2, am and phys1 are kept opaque, so that each address is one shift
+    // (and add) of the field the cost read uses too, rather than a shift and
+    // a mask of the word of its own
+    uint32_t i2 = __builtin_amdgcn_alignbit(hi, lo, 25) & 0x7FFu;
+    asm("" : "+v"(i2));
+    uint32_t am = i2 * 8u + 8u * tetra::kMidOffset;                   // 8 * (808 + i2), bit 14 = delta
+    asm("" : "+v"(am));
+    uint32_t a1;                                                      // 8 * phys1
+    uint32_t phys1 = 0;
+    if constexpr (Cost) {
+        phys1 = (lo >> 13) & 0xFFFu;
+        asm("" : "+v"(phys1));
+        a1 = phys1 << 3;
+    } else {
+        a1 = (lo >> 10) & 0x7FF8u;
+    }
     const uint32_t u3 = (hi >> 1) & 0x7FF8u;                          // 8 * ((p ^ r) << 11 | i3')
     const uint32_t a3 = u3 ^ (am & 0x4000u);                          // 8 * phys3 (Eq. 3)
     BlockFetch f;
@@ -149,8 +162,8 @@ __device__ __forceinline__ BlockFetch fetch_block(uint32_t lo, uint32_t hi, lds_
     f.r[4] = r2.x;
     f.r[5] = r2.y;
     if constexpr (Cost) {
-        cost[0] = L[kCostOff + (a1 >> 3)];
-        cost[1] = L[kCostOff + (am >> 3)];
+        cost[0] = L[kCostOff + phys1];
+        cost[1] = L[kCostOff + tetra::kMidOffset + i2];
         cost[2] = L[kCostOff + (a3 >> 3)];
     }
     return f;
